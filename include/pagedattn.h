@@ -1,0 +1,164 @@
+/*
+ * pagedattn.h -- C ABI of the MI355X (gfx950) paged-KV grouped-query
+ * attention library (libpagedattn.so).
+ *
+ * The operation is the decode-step attention of MoE-Lens (arXiv 2504.09345):
+ * every sequence of a batch attends with its query heads to its own cached
+ * keys and values, which live in fixed-size blocks of token slots addressed
+ * through a per-sequence block table (Sec. 5.5, the paged-KV assumption of
+ * the Stage-2 model).  A group of s = H_q / H_kv query heads shares one KV head
+ * (grouped-query attention, Sec. 2); query head h reads KV head h / s.  KV is
+ * stored in bf16 and the arithmetic runs in fp32 as dot products q.k and
+ * scaled vector adds over V (Sec. 5.3, Eq. 6 and the text after it).  The new
+ * token's K/V are already in the cache when decode attention runs (Sec. 6.4,
+ * compute-graph division), so a context length counts the current token.
+ * The varlen entry adds causal prefill chunks that share the launch with the
+ * decode rows (the paper prefills on the GPU, Sec. 6.4; chunking is this
+ * library's reading: a chunk's own K/V are already in its pages).
+ *
+ * Result, per sequence b, query row r of its chunk of length L (decode: L = 1,
+ * r = 0) and query head h, with C = context_lens[b] and g = h / s:
+ *   x_t = scale * dot(q[row][h], K[t])           for t = 0 .. C - L + r
+ *   out[row][h] = sum_t softmax(x)_t * V[t]
+ * where K[t] / V[t] is slot t % P of page block_table[b][t / P], KV head g.
+ * A row that sees no key (C = 0) produces zeros.
+ *
+ * Conventions for every entry point
+ *   - All array pointers are DEVICE pointers (HBM), except where a name ends
+ *     in _host.  The caller owns every buffer; the library allocates nothing
+ *     and keeps no state between calls, so calls on different streams may
+ *     overlap as long as their output and workspace buffers do not.
+ *   - Work is enqueued on `stream` (NULL = the null stream) and the call
+ *     returns without synchronising.  Faults inside kernels (for example a
+ *     block-table entry outside the pool) surface at the caller's next
+ *     synchronisation; the hot path does not range-check page indices.
+ *   - Argument validation happens on the host before any HIP call; a
+ *     validation failure enqueues nothing.
+ *   - Return value: PA_OK (0) or a negative error code (see pa_strerror).
+ *
+ * Layouts (row-major, element type given by dims->dtype for q/k/v/out):
+ *   q, out        [num_q_rows][num_q_heads][head_dim]
+ *                 (decode: num_q_rows = num_seqs, row b belongs to sequence b)
+ *   k_pages,
+ *   v_pages       [num_pages][num_kv_heads][page_size][head_dim]
+ *                 one (page, kv head) tile is page_size*head_dim contiguous
+ *                 elements (4 KiB at 16 x 128 bf16)
+ *   block_table   int32 [num_seqs][max_pages_per_seq]; entries at or beyond
+ *                 ceil(context_lens[b] / page_size) are never read
+ *   context_lens  int32 [num_seqs], 0 <= context_lens[b] <= max_context_len
+ *   query_start_loc int32 [num_seqs + 1] (varlen only): sequence b owns rows
+ *                 query_start_loc[b] .. query_start_loc[b+1]-1, with
+ *                 query_start_loc[0] = 0 and
+ *                 1 <= L_b = query_start_loc[b+1]-query_start_loc[b]
+ *                    <= min(max_q_len, context_lens[b])  (or L_b = 0 when
+ *                 context_lens[b] = 0)
+ */
+#ifndef PAGEDATTN_H
+#define PAGEDATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Error codes. */
+enum {
+  PA_OK = 0,
+  PA_EINVAL = -1,  /* null pointer, negative or inconsistent size */
+  PA_ENOTSUP = -2, /* head_dim, page_size, dtype or GQA group size not compiled */
+  PA_ENOSPC = -3,  /* workspace smaller than pa_workspace_size() */
+  PA_EHIP = -4     /* a HIP launch reported an error (hipGetLastError) */
+};
+
+/* Element type of q, k_pages, v_pages and out (all four share it).  bf16 is
+ * stored as raw 16-bit patterns; out is rounded to nearest even from fp32. */
+typedef enum { PA_BF16 = 0, PA_FP32 = 1 } pa_dtype_t;
+
+/* Problem description (host memory, read during the call only).
+ * Supported: head_dim 64 or 128; page_size 16; GQA group size
+ * s = num_q_heads / num_kv_heads in {1, 2, 4, 6, 8}; dtype bf16 or fp32. */
+typedef struct pa_dims {
+  int32_t num_seqs;          /* B >= 0                                      */
+  int32_t num_q_heads;       /* H_q > 0, a multiple of num_kv_heads         */
+  int32_t num_kv_heads;      /* H_kv > 0                                    */
+  int32_t head_dim;          /* D                                           */
+  int32_t page_size;         /* token slots per page, must be 16            */
+  int32_t num_pages;         /* pages in the pool                           */
+  int32_t max_pages_per_seq; /* block_table row stride, >= ceil(max_context_len / 16) */
+  int32_t max_context_len;   /* upper bound on context_lens[], sizes the grid */
+  int32_t pages_per_split;   /* split-K granule in pages; 0 = library default */
+  int32_t dtype;             /* pa_dtype_t                                  */
+  int32_t num_q_rows;        /* varlen: total query rows; decode: 0 or num_seqs */
+  int32_t max_q_len;         /* varlen: bound on any chunk length; decode: 0 or 1 */
+} pa_dims_t;
+
+/* Optional timing hooks: when a pa_timing_t* is passed and an event is
+ * non-NULL, it is recorded on the call's stream at that point.  attn_begin
+ * before the attention kernel, attn_end right after it, reduce_end after the
+ * split-K reduction (recorded even when no reduction was needed). */
+typedef struct pa_timing {
+  hipEvent_t attn_begin;
+  hipEvent_t attn_end;
+  hipEvent_t reduce_end;
+} pa_timing_t;
+
+/* Bytes of device workspace a paged_attn / paged_attn_varlen call with these
+ * dims needs (split-K partial outputs and softmax statistics, plus the varlen
+ * work list).  Writes 0 when no workspace is needed.  Host only; no HIP call.
+ * Errors: PA_EINVAL / PA_ENOTSUP as for paged_attn. */
+int pa_workspace_size(const pa_dims_t *dims, size_t *bytes);
+
+/* Decode attention: one query row per sequence (Sec. 6.6 computes exactly
+ * this on the CPU; here it is a split-K HIP kernel plus a reduction kernel).
+ *   q            [num_seqs][H_q][D]        device, read
+ *   k_pages,
+ *   v_pages      pool, see layouts above   device, read
+ *   block_table, context_lens              device, read
+ *   scale        multiplies every dot product (typically 1/sqrt(D))
+ *   out          [num_seqs][H_q][D]        device, written
+ *   workspace    device scratch of at least pa_workspace_size() bytes (may
+ *                be NULL when that size is 0); contents are overwritten
+ *   timing       optional events, may be NULL
+ * Errors: PA_EINVAL, PA_ENOTSUP, PA_ENOSPC, PA_EHIP. */
+int paged_attn(const void *q, const void *k_pages, const void *v_pages,
+               const int32_t *block_table, const int32_t *context_lens, float scale,
+               void *out, const pa_dims_t *dims, void *workspace, size_t workspace_bytes,
+               hipStream_t stream, const pa_timing_t *timing);
+
+/* Mixed batch: causal prefill chunks and decode rows in one launch.
+ * Same as paged_attn, with q/out of [num_q_rows][H_q][D] and the device array
+ * query_start_loc (see layouts).  Row j of a chunk of length L in a sequence
+ * of context C attends to positions 0 .. C - L + j.  dims->num_q_rows must
+ * equal query_start_loc[num_seqs] and dims->max_q_len bound every L_b.
+ * Errors: PA_EINVAL, PA_ENOTSUP, PA_ENOSPC, PA_EHIP. */
+int paged_attn_varlen(const void *q, const void *k_pages, const void *v_pages,
+                      const int32_t *block_table, const int32_t *context_lens,
+                      const int32_t *query_start_loc, float scale, void *out,
+                      const pa_dims_t *dims, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream, const pa_timing_t *timing);
+
+/* Block-table gather trace: for every cached token, sequence-major, the flat
+ * pool row page * page_size + slot that the attention kernels read for it
+ * (computed by the same device address function the kernels use).
+ *   rows_out  int64 device array of sum_b context_lens[b] entries; sequence b
+ *             starts at sum_{b' < b} context_lens[b'].
+ *   row_start int64 device array of num_seqs entries holding those starts
+ *             (the caller computes them; the library does not scan).
+ * Uses num_seqs, page_size, max_pages_per_seq, max_context_len of dims.
+ * Errors: PA_EINVAL, PA_ENOTSUP, PA_EHIP. */
+int pa_gather_trace(const int32_t *block_table, const int32_t *context_lens,
+                    const int64_t *row_start, const pa_dims_t *dims, int64_t *rows_out,
+                    hipStream_t stream);
+
+/* Static description of an error code (never NULL). */
+const char *pa_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAGEDATTN_H */

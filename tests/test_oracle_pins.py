@@ -1,0 +1,307 @@
+"""Pins of the CPU oracle against facts fixed by the mathematics, independent
+of the oracle's own code: a library routine on a dense layout, invariances,
+closed forms, brute force on tiny inputs and a hand-derived gather fixture.
+
+The attention being defined is the paged GQA decode attention of MoE-Lens
+(arXiv 2504.09345): paged KV blocks (Sec. 5.5), grouped-query heads (Sec. 2),
+bf16 storage with fp32 arithmetic (Sec. 5.3, Eq. 6), causal prefill chunks
+(the library's reading of Sec. 6.4).  The paper prints no worked attention
+example, so no pin comes from printed attention values.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2504_09345_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _f32(a):
+    return W.bf16_bits_to_f32(a) if a.dtype == np.uint16 else a.astype(np.float32)
+
+
+def _dense_sdpa_f64(batch):
+    """torch SDPA (float64, CPU) on the identity-layout pool reshaped to dense
+    per-sequence K/V: no block-table gather is involved."""
+    B, H_q, H_kv, D = batch.num_seqs, batch.num_q_heads, batch.num_kv_heads, batch.head_dim
+    mp, P = batch.max_pages_per_seq, W.PAGE_SIZE
+    s = H_q // H_kv
+    k = torch.from_numpy(_f32(batch.k_pages)).double()
+    v = torch.from_numpy(_f32(batch.v_pages)).double()
+    # [B*mp][H_kv][P][D] -> [B][H_kv][mp*P][D]
+    k = k.reshape(B, mp, H_kv, P, D).permute(0, 2, 1, 3, 4).reshape(B, H_kv, mp * P, D)
+    v = v.reshape(B, mp, H_kv, P, D).permute(0, 2, 1, 3, 4).reshape(B, H_kv, mp * P, D)
+    q_all = torch.from_numpy(_f32(batch.q)).double()
+    qsl = batch.query_start_loc if batch.query_start_loc is not None else np.arange(B + 1)
+    out = torch.zeros_like(q_all)
+    for b in range(B):
+        C = int(batch.context_lens[b])
+        r0, r1 = int(qsl[b]), int(qsl[b + 1])
+        L = r1 - r0
+        if C == 0 or L == 0:
+            continue
+        qb = q_all[r0:r1].permute(1, 0, 2).unsqueeze(0)            # [1][H_q][L][D]
+        kb = k[b, :, :C].repeat_interleave(s, dim=0).unsqueeze(0)  # [1][H_q][C][D]
+        vb = v[b, :, :C].repeat_interleave(s, dim=0).unsqueeze(0)
+        pos = torch.arange(C - L, C).unsqueeze(1)                  # absolute query positions
+        mask = torch.arange(C).unsqueeze(0) <= pos                 # [L][C]
+        ob = torch.nn.functional.scaled_dot_product_attention(qb, kb, vb, attn_mask=mask,
+                                                              scale=batch.scale)
+        out[r0:r1] = ob[0].permute(1, 0, 2)
+    return out.numpy()
+
+
+def _run_oracle(batch):
+    if batch.query_start_loc is None:
+        return oracle.paged_attn(batch.q, batch.k_pages, batch.v_pages, batch.block_table,
+                                 batch.context_lens, batch.scale)
+    return oracle.paged_attn_varlen(batch.q, batch.k_pages, batch.v_pages, batch.block_table,
+                                    batch.context_lens, batch.query_start_loc, batch.scale)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("H_q,H_kv,D", [(8, 2, 64), (6, 6, 64), (12, 2, 128), (4, 1, 32)])
+def test_decode_equals_dense_sdpa(dtype, H_q, H_kv, D):
+    ctx = [1, 16, 17, 37, 100]
+    batch = W.identity_layout(len(ctx), ctx, H_q, H_kv, D, seed=11, dtype=dtype)
+    got = _run_oracle(batch)
+    ref = _dense_sdpa_f64(batch)
+    np.testing.assert_allclose(got, ref, rtol=2e-5, atol=2e-6)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_prefill_chunks_equal_dense_causal_sdpa(dtype):
+    # chunk lengths with prior context 0 (plain causal), partial and decode rows
+    ctx = [40, 70, 33, 9, 64]
+    qlen = [40, 21, 1, 9, 17]
+    batch = W.identity_layout(len(ctx), ctx, 8, 2, 64, seed=5, dtype=dtype, qlen=qlen)
+    got = _run_oracle(batch)
+    ref = _dense_sdpa_f64(batch)
+    np.testing.assert_allclose(got, ref, rtol=2e-5, atol=2e-6)
+
+
+def test_prefill_prior_zero_is_plain_causal():
+    # with no prior context the chunk is ordinary causal self-attention: SDPA's
+    # own is_causal path (top-left aligned) must agree
+    ctx, L = [48], [48]
+    batch = W.identity_layout(1, ctx, 4, 2, 64, seed=8, dtype="fp32", qlen=L)
+    got = _run_oracle(batch)
+    k = torch.from_numpy(batch.k_pages).double().reshape(3, 2, 16, 64).permute(1, 0, 2, 3)
+    k = k.reshape(2, 48, 64).repeat_interleave(2, dim=0)[None]
+    v = torch.from_numpy(batch.v_pages).double().reshape(3, 2, 16, 64).permute(1, 0, 2, 3)
+    v = v.reshape(2, 48, 64).repeat_interleave(2, dim=0)[None]
+    q = torch.from_numpy(batch.q).double().permute(1, 0, 2)[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True,
+                                                           scale=batch.scale)
+    np.testing.assert_allclose(got, ref[0].permute(1, 0, 2).numpy(), rtol=2e-5, atol=2e-6)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_page_permutation_invariance_bit_exact(dtype):
+    batch = W.generate("tiny", seed=3, dtype=dtype)
+    a = _run_oracle(batch)
+    for s in (1, 2):
+        b = _run_oracle(W.permute_pages(batch, seed=100 + s))
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_one_token_context_returns_v_exactly(dtype):
+    batch = W.generate("tiny", seed=4, dtype=dtype)
+    batch.context_lens[:] = 1
+    out = _run_oracle(batch)
+    s = batch.num_q_heads // batch.num_kv_heads
+    for b in range(batch.num_seqs):
+        page = batch.block_table[b, 0]
+        for h in range(batch.num_q_heads):
+            v0 = _f32(batch.v_pages[page, h // s, 0])
+            assert np.array_equal(out[b, h].view(np.uint32), v0.view(np.uint32))
+
+
+def _brute_weights(batch, b, h, L=1, r=0, qrow=None):
+    """float64 softmax weights with math.exp, pure Python loops (tiny only)."""
+    s = batch.num_q_heads // batch.num_kv_heads
+    g = h // s
+    C = int(batch.context_lens[b])
+    qrow = b if qrow is None else qrow
+    qv = [float(x) for x in _f32(batch.q[qrow, h])]
+    xs = []
+    for t in range(C - L + r + 1):
+        page = int(batch.block_table[b, t // 16])
+        kv = _f32(batch.k_pages[page, g, t % 16])
+        xs.append(sum(qv[d] * float(kv[d]) for d in range(len(qv))) * batch.scale)
+    m = max(xs)
+    e = [math.exp(x - m) for x in xs]
+    tot = sum(e)
+    return [x / tot for x in e]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_softmax_weights_sum_to_one_and_match_brute_force(dtype):
+    batch = W.generate("tiny", seed=6, dtype=dtype)
+    for b in range(batch.num_seqs):
+        for h in (0, 3, 5, 7):
+            w = oracle.softmax_weights(batch.q, batch.k_pages, batch.block_table,
+                                       batch.context_lens, batch.scale, b, h)
+            assert w.shape[0] == batch.context_lens[b]
+            assert abs(float(np.sum(w, dtype=np.float64)) - 1.0) < 1e-6
+            ref = np.array(_brute_weights(batch, b, h))
+            np.testing.assert_allclose(w, ref, rtol=1e-6, atol=1e-9)
+
+
+def test_softmax_weights_prefill_row_brute_force():
+    batch = W.identity_layout(1, [50], 4, 2, 64, seed=2, dtype="bf16", qlen=[20])
+    for r in (0, 7, 19):
+        w = oracle.softmax_weights(batch.q, batch.k_pages, batch.block_table,
+                                   batch.context_lens, batch.scale, 0, 3, L=20, r=r, qrow=r)
+        assert w.shape[0] == 50 - 20 + r + 1
+        np.testing.assert_allclose(w, _brute_weights(batch, 0, 3, L=20, r=r, qrow=r),
+                                   rtol=1e-6, atol=1e-9)
+
+
+def test_constant_v_returns_that_vector():
+    batch = W.generate("tiny", seed=7, dtype="fp32")
+    # every token of (page, kv head) g gets the same V row, per kv head
+    rows = np.random.default_rng(1).standard_normal((batch.num_kv_heads, batch.head_dim))
+    batch.v_pages[:] = rows.astype(np.float32)[None, :, None, :]
+    out = _run_oracle(batch)
+    s = batch.num_q_heads // batch.num_kv_heads
+    for h in range(batch.num_q_heads):
+        np.testing.assert_allclose(out[:, h], np.broadcast_to(rows[h // s], out[:, h].shape),
+                                   rtol=2e-6, atol=1e-7)
+
+
+@pytest.mark.parametrize("zero", ["q", "scale"])
+def test_zero_logits_give_mean_of_visible_v(zero):
+    batch = W.generate("tiny", seed=9, dtype="fp32")
+    if zero == "q":
+        batch.q[:] = 0
+    else:
+        batch.scale = 0.0
+    out = _run_oracle(batch)
+    s = batch.num_q_heads // batch.num_kv_heads
+    for b in range(batch.num_seqs):
+        C = int(batch.context_lens[b])
+        pages = batch.block_table[b, : (C + 15) // 16]
+        vv = batch.v_pages[pages].astype(np.float64)             # [np][H_kv][16][D]
+        vv = vv.transpose(1, 0, 2, 3).reshape(batch.num_kv_heads, -1, batch.head_dim)[:, :C]
+        mean = vv.mean(axis=1)
+        for h in range(batch.num_q_heads):
+            np.testing.assert_allclose(out[b, h], mean[h // s], rtol=1e-5, atol=1e-6)
+
+
+def test_large_scale_selects_argmax_value_row():
+    batch = W.generate("tiny", seed=10, dtype="fp32")
+    batch.scale = 1.0e4
+    out = _run_oracle(batch)
+    s = batch.num_q_heads // batch.num_kv_heads
+    checked = 0
+    for b in range(batch.num_seqs):
+        C = int(batch.context_lens[b])
+        for h in range(batch.num_q_heads):
+            g = h // s
+            logits, vals = [], []
+            for t in range(C):
+                page = batch.block_table[b, t // 16]
+                logits.append(float(np.dot(batch.q[b, h].astype(np.float64),
+                                           batch.k_pages[page, g, t % 16].astype(np.float64))))
+                vals.append(batch.v_pages[page, g, t % 16])
+            order = np.argsort(logits)
+            if logits[order[-1]] - logits[order[-2]] < 0.05:  # need a clear winner
+                continue
+            np.testing.assert_array_equal(out[b, h], vals[order[-1]])
+            checked += 1
+    assert checked > 16
+
+
+def test_single_row_chunks_equal_decode_and_last_chunk_row_equals_decode():
+    batch = W.identity_layout(3, [30, 64, 81], 8, 2, 64, seed=12, dtype="bf16", qlen=[12, 1, 30])
+    full = _run_oracle(batch)
+    qsl = batch.query_start_loc
+    # decode at the same context with the chunk's last query row
+    last_rows = batch.q[qsl[1:] - 1]
+    dec = oracle.paged_attn(last_rows, batch.k_pages, batch.v_pages, batch.block_table,
+                            batch.context_lens, batch.scale)
+    assert np.array_equal(full[qsl[1:] - 1].view(np.uint32), dec.view(np.uint32))
+    # a chunk row j equals decode over a context cut at its own position
+    ctx_cut = batch.context_lens.copy()
+    ctx_cut[2] = 81 - 30 + 5 + 1
+    dec5 = oracle.paged_attn(batch.q[qsl[:-1] + np.array([0, 0, 5])], batch.k_pages,
+                             batch.v_pages, batch.block_table, ctx_cut, batch.scale)
+    assert np.array_equal(full[qsl[2] + 5].view(np.uint32), dec5[2].view(np.uint32))
+
+
+def test_empty_context_gives_zeros():
+    batch = W.generate("tiny", seed=13, dtype="bf16")
+    batch.context_lens[1] = 0
+    out = _run_oracle(batch)
+    assert np.all(out[1] == 0)
+    assert np.all(np.isfinite(out))
+
+
+def test_poisoned_pool_does_not_leak():
+    a = _run_oracle(W.generate("tiny", seed=14, dtype="bf16"))
+    b = _run_oracle(W.generate("tiny", seed=14, dtype="bf16", poison=True))
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def _read_gather_fixture():
+    path = os.path.join(GOLDEN, "gather_tiny.txt")
+    sec, data = None, {}
+    with open(path) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if not line:
+                continue
+            if line.endswith(":"):
+                sec = line[:-1]
+                data[sec] = []
+            else:
+                data[sec].append([int(x) for x in line.split()])
+    return data
+
+
+def test_gather_indices_hand_fixture():
+    fx = _read_gather_fixture()
+    bt = np.array(fx["block_table"], np.int32)
+    ctx = np.array(fx["context_lens"][0], np.int32)
+    rows = oracle.gather_indices(bt, ctx, 16, int(fx["num_pages"][0][0]))
+    expect = np.array([x for r in fx["rows"] for x in r], np.int64)
+    assert np.array_equal(rows, expect)
+
+
+def test_gather_indices_identity_and_permuted():
+    batch = W.identity_layout(3, [5, 16, 40], 2, 1, 8, seed=0)
+    rows = oracle.gather_indices(batch.block_table, batch.context_lens, 16, batch.num_pages)
+    mp = batch.max_pages_per_seq
+    expect = np.concatenate([b * mp * 16 + np.arange(c) for b, c in enumerate([5, 16, 40])])
+    assert np.array_equal(rows, expect)
+    perm = W.permute_pages(batch, seed=3)
+    prow = oracle.gather_indices(perm.block_table, perm.context_lens, 16, perm.num_pages)
+    # permuted rows hold the same token data as the identity rows
+    flat_id = batch.k_pages.transpose(0, 2, 1, 3).reshape(-1, batch.num_kv_heads * batch.head_dim)
+    flat_pm = perm.k_pages.transpose(0, 2, 1, 3).reshape(-1, perm.num_kv_heads * perm.head_dim)
+    assert np.array_equal(flat_id[rows], flat_pm[prow])
+    assert len(np.unique(prow)) == len(prow)
+
+
+def test_oracle_rejects_out_of_pool_page():
+    batch = W.generate("tiny", seed=1)
+    batch.block_table[0, 0] = batch.num_pages
+    with pytest.raises(ValueError):
+        _run_oracle(batch)
+
+
+def test_oracle_thread_count_does_not_change_result():
+    batch = W.generate("tiny", seed=15, dtype="bf16")
+    oracle.set_threads(1)
+    a = _run_oracle(batch)
+    oracle.set_threads(4)
+    b = _run_oracle(batch)
+    oracle.set_threads(0)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
