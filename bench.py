@@ -1,0 +1,298 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged GQA decode-attention hot path on one MI355X.
+
+One step = one paged_attn call (split-K attention kernel + split reduction)
+over a whole synthetic decode batch whose inputs are already resident in HBM.
+Default workload: Mixtral-8x7B-shaped decode, batch 256, 32 query / 8 KV
+heads, head dim 128, bf16 KV, page size 16, context lengths uniform in
+[512, 2048], pages randomly placed in a pool 1.25x the need.
+
+Prints ONE JSON line: seqs/s for the whole job, the attention kernel's
+achieved KV bandwidth against the MI355X HBM peak (roofline), and the CPU
+oracle timed on this host's cores on a bounded sample as a reported baseline.
+
+Timing: W warm-up steps, then exactly K timed steps bracketed by device
+synchronisation.  The K/V pools are replicated R times and the steps rotate
+through the copies, so each step streams its KV from HBM and not from the
+256 MB last-level cache left warm by the previous step.  The attention
+kernel's own duration is measured with HIP events the library records on the
+launch stream around that kernel.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2504_09345_amd import binding as pb  # noqa: E402
+from paper_2504_09345_amd import workloads as W  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD public figure
+METRIC = "decode attention seqs/sec and achieved KV GB/s (% of MI355X HBM peak)"
+WORKLOAD_NAMES = {
+    "mixtral-256": "mixtral-8x7b-decode-b256-ctx512-2048",
+    "long-ctx-64": "mixtral-8x7b-decode-b64-ctx8192-32768",
+    "dbrx-512": "dbrx-decode-b512-lognormal-ctx128-8192",
+    "mixed": "mixtral-8x7b-mixed-8x512prefill-512decode",
+    "tiny": "tiny-decode-b4",
+}
+
+
+def elem_bytes(dtype: str) -> int:
+    return 2 if dtype == "bf16" else 4
+
+
+def kv_bytes_per_token(num_kv_heads: int, head_dim: int, elem: int) -> int:
+    """K and V of one token of one layer: H_kv * D elements each."""
+    return 2 * num_kv_heads * head_dim * elem
+
+
+def algorithmic_bytes(b: W.Batch) -> dict:
+    """Bytes the method must move per launch: every cached token's K and V once
+    (valid tokens only), q and out once, the block-table entries and lengths
+    read.  Page padding and split-K partials are overhead, not counted."""
+    e = elem_bytes(b.dtype)
+    ctx = b.context_lens.astype(np.int64)
+    kv = int(ctx.sum()) * kv_bytes_per_token(b.num_kv_heads, b.head_dim, e)
+    qo = 2 * b.num_q_rows * b.num_q_heads * b.head_dim * e
+    meta = int(((ctx + 15) // 16).sum()) * 4 + 4 * b.num_seqs
+    if b.query_start_loc is not None:
+        meta += 4 * (b.num_seqs + 1)
+    return dict(kv=kv, q_out=qo, meta=meta, total=kv + qo + meta)
+
+
+def algorithmic_flops(b: W.Batch) -> int:
+    """QK (2D) and PV (2D) per query head per visible key."""
+    ql = b.q_lens.astype(np.int64)
+    ctx = b.context_lens.astype(np.int64)
+    # visible keys summed over a chunk: sum_{r<L} (C - L + r + 1)
+    vis = ql * ctx - ql * (ql - 1) // 2
+    return int(4 * b.head_dim * b.num_q_heads * vis.sum())
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch itself uses."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        e = ctypes.c_void_p()
+        if self.lib.hipEventCreate(ctypes.byref(e)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return e.value
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def destroy(self, e):
+        self.lib.hipEventDestroy(e)
+
+
+def to_device(a: np.ndarray, torch):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _cpu_baseline(batch: W.Batch, target_s: float, max_seqs: int | None):
+    import oracle
+    B = batch.num_seqs
+    n = max(1, min(B, 8))
+    limit = B if max_seqs is None else min(B, max_seqs)
+
+    def sub(n):
+        if batch.query_start_loc is None:
+            return (batch.q[:n], batch.block_table[:n], batch.context_lens[:n], None)
+        qsl = batch.query_start_loc[: n + 1]
+        return (batch.q[: qsl[-1]], batch.block_table[:n], batch.context_lens[:n], qsl)
+
+    def run(n):
+        q, bt, cl, qsl = sub(n)
+        t0 = time.perf_counter()
+        if qsl is None:
+            oracle.paged_attn(q, batch.k_pages, batch.v_pages, bt, cl, batch.scale)
+        else:
+            oracle.paged_attn_varlen(q, batch.k_pages, batch.v_pages, bt, cl, qsl, batch.scale)
+        return time.perf_counter() - t0
+
+    dt = run(n)
+    while dt < target_s / 3 and n < limit:
+        n = min(limit, max(n + 1, int(n * min(8.0, (target_s / 3) / max(dt, 1e-3)))))
+        dt = run(n)
+    reps = max(1, min(3, int(target_s / max(dt, 1e-3))))
+    times = [dt] + [run(n) for _ in range(reps - 1)]
+    t = float(np.median(times))
+    return dict(value=n / t, unit="seqs/s", cores=oracle.get_threads(), kind="oracle",
+                sample=f"first {n} of {B} sequences of the same batch, median of {len(times)} runs "
+                       f"of {t:.2f} s (fp32 oracle, OpenMP)")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral-256", choices=sorted(W.CONFIGS))
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--pages-per-split", type=int, default=0)
+    ap.add_argument("--rotate", type=int, default=0,
+                    help="pool copies to rotate through (0: enough for >= 1.5 GB per copy set)")
+    ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one device copy of this many MiB before timing "
+                         "(a known-size kernel for scaling profiler byte counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the attention of one "
+                                   "GPU's share is measured; --gpus must be 1"}))
+        return 2
+
+    import torch
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        return 2
+    pb.load()  # fail loudly if the HIP library is missing
+
+    t_gen = time.perf_counter()
+    batch = W.generate(args.workload, seed=args.seed, dtype="bf16")
+    gen_s = time.perf_counter() - t_gen
+    dev_q = to_device(batch.q, torch)
+    bt = to_device(batch.block_table, torch)
+    cl = to_device(batch.context_lens, torch)
+    qsl = to_device(batch.query_start_loc, torch) if batch.query_start_loc is not None else None
+    out = torch.empty_like(dev_q)
+
+    pool_bytes = 2 * batch.k_pages.nbytes
+    R = args.rotate or max(2, int(np.ceil(1.5e9 / pool_bytes)))
+    k0, v0 = to_device(batch.k_pages, torch), to_device(batch.v_pages, torch)
+    pools = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(R - 1)]
+
+    mcl = int(batch.context_lens.max())
+    if qsl is None:
+        dims = pb.make_dims(dev_q, k0, bt, mcl, args.pages_per_split)
+    else:
+        dims = pb.make_dims(dev_q, k0, bt, mcl, args.pages_per_split,
+                            num_q_rows=batch.num_q_rows, max_q_len=int(batch.q_lens.max()))
+    ws_bytes = pb.pa_workspace_size(dims)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    ev = HipEvents()
+    K, Wm = args.steps, args.warmup
+    marks = [pb.PaTiming(ev.create(), ev.create(), ev.create()) for _ in range(K)]
+
+    def step(i, timing=None):
+        k, v = pools[i % R]
+        if qsl is None:
+            pb.paged_attn(dev_q, k, v, bt, cl, batch.scale, out, dims, ws, stream, timing)
+        else:
+            pb.paged_attn_varlen(dev_q, k, v, bt, cl, qsl, batch.scale, out, dims, ws, stream,
+                                 timing)
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20)
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    for i in range(Wm):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(Wm + i, marks[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    attn_ms = [ev.elapsed_ms(m.attn_begin, m.attn_end) for m in marks]
+    red_ms = [ev.elapsed_ms(m.attn_end, m.reduce_end) for m in marks]
+    step_ms = [ev.elapsed_ms(m.attn_begin, m.reduce_end) for m in marks]
+    for m in marks:
+        ev.destroy(m.attn_begin), ev.destroy(m.attn_end), ev.destroy(m.reduce_end)
+
+    by = algorithmic_bytes(batch)
+    fl = algorithmic_flops(batch)
+    attn_avg_s = float(np.mean(attn_ms)) / 1e3
+    achieved = by["total"] / attn_avg_s / 1e9
+    value = batch.num_seqs * K / wall
+    ms_per_step = wall / K * 1e3
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "seqs/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD_NAMES.get(args.workload, args.workload),
+            "num_seqs": batch.num_seqs, "num_q_heads": batch.num_q_heads,
+            "num_kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim, "page_size": 16,
+            "context_len_total": int(batch.context_lens.sum()),
+            "pages_per_split": args.pages_per_split, "seed": args.seed, "pool_copies": R,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+        },
+        "kernels": {
+            "attention_us_mean": round(float(np.mean(attn_ms)) * 1e3, 2),
+            "attention_us_median": round(float(np.median(attn_ms)) * 1e3, 2),
+            "reduce_us_mean": round(float(np.mean(red_ms)) * 1e3, 2),
+            "step_us_median": round(float(np.median(step_ms)) * 1e3, 2),
+            "kv_gb_per_s_step": round(by["total"] / (float(np.median(step_ms)) / 1e3) / 1e9, 1),
+            "algorithmic_bytes": by,
+            "algorithmic_gflop": round(fl / 1e9, 3),
+            "tflops_attention": round(fl / attn_avg_s / 1e12, 2),
+        },
+        "gen_s": round(gen_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = _cpu_baseline(batch, args.cpu_baseline_seconds, None)
+        res["cpu_baseline"]["host_cpu"] = _cpu_model()
+    print(json.dumps(res))
+    return 0
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+if __name__ == "__main__":
+    sys.exit(main())

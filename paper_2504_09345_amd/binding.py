@@ -1,0 +1,169 @@
+"""ctypes binding of libpagedattn.so, the C ABI declared in include/pagedattn.h.
+
+Argument marshalling only: every step of the attention runs in the library's
+HIP kernels.  Device buffers are passed as torch tensors (torch provides
+device memory and streams here) or as raw integer device addresses.  The
+library is loaded on first use; if it has not been built the call raises
+instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "_lib", "libpagedattn.so")
+
+PA_OK, PA_EINVAL, PA_ENOTSUP, PA_ENOSPC, PA_EHIP = 0, -1, -2, -3, -4
+PA_BF16, PA_FP32 = 0, 1
+PAGE_SIZE = 16
+
+EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "pa_gather_trace",
+            "pa_strerror")
+
+
+class PaDims(ctypes.Structure):
+    """pa_dims_t"""
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "num_seqs", "num_q_heads", "num_kv_heads", "head_dim", "page_size", "num_pages",
+        "max_pages_per_seq", "max_context_len", "pages_per_split", "dtype", "num_q_rows",
+        "max_q_len")]
+
+
+class PaTiming(ctypes.Structure):
+    """pa_timing_t: three hipEvent_t handles (NULL = not recorded)."""
+    _fields_ = [("attn_begin", ctypes.c_void_p), ("attn_end", ctypes.c_void_p),
+                ("reduce_end", ctypes.c_void_p)]
+
+
+class PagedAttnError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} returned {code}: {pa_strerror(code)}")
+        self.code = code
+
+
+_lib = None
+
+
+def load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(there is no fallback path)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, SZ = ctypes.c_void_p, ctypes.c_size_t
+    DP, TP = ctypes.POINTER(PaDims), ctypes.POINTER(PaTiming)
+    lib.pa_workspace_size.argtypes = [DP, ctypes.POINTER(SZ)]
+    lib.pa_workspace_size.restype = ctypes.c_int
+    lib.paged_attn.argtypes = [P, P, P, P, P, ctypes.c_float, P, DP, P, SZ, P, TP]
+    lib.paged_attn.restype = ctypes.c_int
+    lib.paged_attn_varlen.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, DP, P, SZ, P, TP]
+    lib.paged_attn_varlen.restype = ctypes.c_int
+    lib.pa_gather_trace.argtypes = [P, P, P, DP, P, P]
+    lib.pa_gather_trace.restype = ctypes.c_int
+    lib.pa_strerror.argtypes = [ctypes.c_int]
+    lib.pa_strerror.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _addr(x):
+    """Device address of a torch tensor, an int address, or None (NULL)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x or None
+    return x.data_ptr() or None
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream or None
+    if isinstance(stream, int):
+        return stream or None
+    return stream.cuda_stream or None
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        return PA_BF16
+    if t.dtype == torch.float32:
+        return PA_FP32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def make_dims(q, k_pages, block_table, max_context_len, pages_per_split=0, num_q_rows=0,
+              max_q_len=0, num_seqs=None) -> PaDims:
+    """pa_dims_t from tensor shapes: q [rows][H_q][D], k_pages [N][H_kv][16][D],
+    block_table [B][max_pages_per_seq]."""
+    rows, H_q, D = q.shape
+    N, H_kv, P, D2 = k_pages.shape
+    B = block_table.shape[0] if num_seqs is None else num_seqs
+    return PaDims(num_seqs=B, num_q_heads=H_q, num_kv_heads=H_kv, head_dim=D, page_size=P,
+                  num_pages=N, max_pages_per_seq=block_table.shape[1],
+                  max_context_len=int(max_context_len), pages_per_split=int(pages_per_split),
+                  dtype=_dtype_code(q), num_q_rows=int(num_q_rows), max_q_len=int(max_q_len))
+
+
+def pa_workspace_size(dims: PaDims) -> int:
+    n = ctypes.c_size_t(0)
+    rc = load().pa_workspace_size(ctypes.byref(dims), ctypes.byref(n))
+    if rc != PA_OK:
+        raise PagedAttnError("pa_workspace_size", rc)
+    return int(n.value)
+
+
+def pa_strerror(code: int) -> str:
+    return load().pa_strerror(int(code)).decode()
+
+
+def _workspace(dims, workspace, device):
+    need = pa_workspace_size(dims)
+    if workspace is None and need > 0:
+        import torch
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    size = 0 if workspace is None else (workspace.numel() * workspace.element_size()
+                                        if hasattr(workspace, "numel") else need)
+    return workspace, size
+
+
+def paged_attn(q, k_pages, v_pages, block_table, context_lens, scale, out, dims: PaDims,
+               workspace=None, stream=None, timing: PaTiming | None = None, check=True) -> int:
+    """int paged_attn(...): decode attention; out is written in place."""
+    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None))
+    rc = load().paged_attn(_addr(q), _addr(k_pages), _addr(v_pages), _addr(block_table),
+                           _addr(context_lens), float(scale), _addr(out), ctypes.byref(dims),
+                           _addr(ws), ws_bytes, _stream(stream),
+                           ctypes.byref(timing) if timing is not None else None)
+    if check and rc != PA_OK:
+        raise PagedAttnError("paged_attn", rc)
+    return rc
+
+
+def paged_attn_varlen(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out,
+                      dims: PaDims, workspace=None, stream=None, timing: PaTiming | None = None,
+                      check=True) -> int:
+    """int paged_attn_varlen(...): causal prefill chunks plus decode rows."""
+    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None))
+    rc = load().paged_attn_varlen(_addr(q), _addr(k_pages), _addr(v_pages), _addr(block_table),
+                                  _addr(context_lens), _addr(query_start_loc), float(scale),
+                                  _addr(out), ctypes.byref(dims), _addr(ws), ws_bytes,
+                                  _stream(stream),
+                                  ctypes.byref(timing) if timing is not None else None)
+    if check and rc != PA_OK:
+        raise PagedAttnError("paged_attn_varlen", rc)
+    return rc
+
+
+def pa_gather_trace(block_table, context_lens, row_start, dims: PaDims, rows_out, stream=None,
+                    check=True) -> int:
+    """int pa_gather_trace(...): pool row of every cached token."""
+    rc = load().pa_gather_trace(_addr(block_table), _addr(context_lens), _addr(row_start),
+                                ctypes.byref(dims), _addr(rows_out), _stream(stream))
+    if check and rc != PA_OK:
+        raise PagedAttnError("pa_gather_trace", rc)
+    return rc

@@ -1,0 +1,204 @@
+// C ABI of libpagedattn.so: host-side validation, launch planning and
+// dispatch.  Validation runs before any HIP call, so a rejected call enqueues
+// nothing and is testable without a GPU.  The library allocates nothing and
+// keeps no state between calls.
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "pa_kernels.h"
+#include "pagedattn.h"
+
+namespace {
+
+// Default split-K granule: 32 pages = 512 tokens per workgroup (8 pages per
+// wave).  Long contexts get many splits; short ones run unsplit.
+constexpr int kDefaultPagesPerSplit = 32;
+
+struct Plan {
+  int s = 0;
+  int pps = 0;
+  int n_split_slots = 0;
+  int rows = 0;
+  size_t ws_o_bytes = 0;
+  size_t ws_ml_bytes = 0;
+  size_t ws_bytes = 0;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool group_supported(int s) { return s == 1 || s == 2 || s == 4 || s == 6 || s == 8; }
+
+int plan(const pa_dims_t* d, bool varlen, Plan* p) {
+  if (d == nullptr || p == nullptr) return PA_EINVAL;
+  if (d->num_seqs < 0 || d->num_q_heads <= 0 || d->num_kv_heads <= 0 || d->num_pages < 0 ||
+      d->max_pages_per_seq < 0 || d->max_context_len < 0 || d->pages_per_split < 0)
+    return PA_EINVAL;
+  if (d->num_q_heads % d->num_kv_heads != 0) return PA_EINVAL;
+  if (d->dtype != PA_BF16 && d->dtype != PA_FP32) return PA_ENOTSUP;
+  if (d->head_dim != 64 && d->head_dim != 128) return PA_ENOTSUP;
+  if (d->page_size != 16) return PA_ENOTSUP;
+  const int s = d->num_q_heads / d->num_kv_heads;
+  if (!group_supported(s)) return PA_ENOTSUP;
+  const int64_t max_pages = ((int64_t)d->max_context_len + 15) / 16;
+  if (max_pages > d->max_pages_per_seq) return PA_EINVAL;
+  if (d->pages_per_split > pa::kMaxPagesPerSplit) return PA_EINVAL;
+  int rows;
+  if (varlen) {
+    if (d->num_q_rows < 0 || d->max_q_len < 0) return PA_EINVAL;
+    if (d->num_q_rows > 0 && (d->max_q_len < 1 || d->num_seqs == 0)) return PA_EINVAL;
+    if (d->max_q_len > d->max_context_len && d->num_q_rows > 0) return PA_EINVAL;
+    rows = d->num_q_rows;
+  } else {
+    if (!(d->num_q_rows == 0 || d->num_q_rows == d->num_seqs)) return PA_EINVAL;
+    if (!(d->max_q_len == 0 || d->max_q_len == 1)) return PA_EINVAL;
+    rows = d->num_seqs;
+  }
+  p->s = s;
+  p->pps = d->pages_per_split > 0 ? d->pages_per_split : kDefaultPagesPerSplit;
+  p->n_split_slots = (int)((max_pages + p->pps - 1) / p->pps);
+  if (p->n_split_slots < 1) p->n_split_slots = 1;
+  p->rows = rows;
+  if ((int64_t)rows * d->num_kv_heads * p->n_split_slots > 0x7fffffffLL) return PA_ENOTSUP;
+  if (p->n_split_slots > 1) {
+    const size_t items = (size_t)rows * (size_t)d->num_q_heads * (size_t)p->n_split_slots;
+    p->ws_o_bytes = align256(items * (size_t)d->head_dim * sizeof(float));
+    p->ws_ml_bytes = align256(items * 2 * sizeof(float));
+  }
+  p->ws_bytes = p->ws_o_bytes + p->ws_ml_bytes;
+  return PA_OK;
+}
+
+void record(hipEvent_t ev, hipStream_t st) {
+  if (ev != nullptr) (void)hipEventRecord(ev, st);
+}
+
+int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+        const int32_t* context_lens, const int32_t* query_start_loc, float scale, void* out,
+        const pa_dims_t* dims, void* workspace, size_t workspace_bytes, hipStream_t stream,
+        const pa_timing_t* timing, bool varlen) {
+  Plan p;
+  int rc = plan(dims, varlen, &p);
+  if (rc != PA_OK) return rc;
+  if (!isfinite(scale)) return PA_EINVAL;
+  if (p.rows > 0) {
+    if (!q || !k_pages || !v_pages || !block_table || !context_lens || !out) return PA_EINVAL;
+    if (varlen && !query_start_loc) return PA_EINVAL;
+  }
+  if (p.ws_bytes > 0 && (workspace == nullptr || workspace_bytes < p.ws_bytes)) return PA_ENOSPC;
+
+  const hipEvent_t ev_begin = timing ? timing->attn_begin : nullptr;
+  const hipEvent_t ev_attn = timing ? timing->attn_end : nullptr;
+  const hipEvent_t ev_reduce = timing ? timing->reduce_end : nullptr;
+  if (p.rows == 0) {
+    record(ev_begin, stream);
+    record(ev_attn, stream);
+    record(ev_reduce, stream);
+    return PA_OK;
+  }
+
+  pa::DecodeArgs a;
+  a.q = q;
+  a.k_pages = k_pages;
+  a.v_pages = v_pages;
+  a.block_table = block_table;
+  a.context_lens = context_lens;
+  a.query_start_loc = varlen ? query_start_loc : nullptr;
+  a.out = out;
+  a.ws_o = p.ws_bytes ? static_cast<float*>(workspace) : nullptr;
+  a.ws_ml = p.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(workspace) + p.ws_o_bytes) : nullptr;
+  a.bt_stride = dims->max_pages_per_seq;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.B = dims->num_seqs;
+  a.max_context_len = dims->max_context_len;
+  a.H_q = dims->num_q_heads;
+  a.H_kv = dims->num_kv_heads;
+  a.pages_per_split = p.pps;
+  a.n_split_slots = p.n_split_slots;
+
+  record(ev_begin, stream);
+  hipError_t e = pa::launch_decode(dims->dtype, dims->head_dim, p.s, a, p.rows, stream);
+  if (e != hipSuccess) return PA_EHIP;
+  record(ev_attn, stream);
+  if (p.n_split_slots > 1) {
+    pa::ReduceArgs r;
+    r.ws_o = a.ws_o;
+    r.ws_ml = a.ws_ml;
+    r.context_lens = context_lens;
+    r.query_start_loc = a.query_start_loc;
+    r.out = out;
+    r.B = dims->num_seqs;
+    r.rows = p.rows;
+    r.H_q = dims->num_q_heads;
+    r.max_context_len = dims->max_context_len;
+    r.pages_per_split = p.pps;
+    r.n_split_slots = p.n_split_slots;
+    e = pa::launch_reduce(dims->dtype, dims->head_dim, r, stream);
+    if (e != hipSuccess) return PA_EHIP;
+  }
+  record(ev_reduce, stream);
+  return PA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int pa_workspace_size(const pa_dims_t* dims, size_t* bytes) {
+  if (bytes == nullptr) return PA_EINVAL;
+  // The workspace depends on the number of query rows only: a call whose
+  // dims carry chunked rows (max_q_len > 1 or num_q_rows != num_seqs) is
+  // planned as varlen, any other as decode (they coincide when all L_b = 1).
+  Plan p;
+  const bool varlen = dims != nullptr &&
+                      (dims->max_q_len > 1 || (dims->num_q_rows != 0 && dims->num_q_rows != dims->num_seqs));
+  int rc = plan(dims, varlen, &p);
+  if (rc != PA_OK) return rc;
+  *bytes = p.ws_bytes;
+  return PA_OK;
+}
+
+int paged_attn(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+               const int32_t* context_lens, float scale, void* out, const pa_dims_t* dims,
+               void* workspace, size_t workspace_bytes, hipStream_t stream,
+               const pa_timing_t* timing) {
+  return run(q, k_pages, v_pages, block_table, context_lens, nullptr, scale, out, dims, workspace,
+             workspace_bytes, stream, timing, false);
+}
+
+int paged_attn_varlen(const void* q, const void* k_pages, const void* v_pages,
+                      const int32_t* block_table, const int32_t* context_lens,
+                      const int32_t* query_start_loc, float scale, void* out,
+                      const pa_dims_t* dims, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream, const pa_timing_t* timing) {
+  return run(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out, dims,
+             workspace, workspace_bytes, stream, timing, true);
+}
+
+int pa_gather_trace(const int32_t* block_table, const int32_t* context_lens,
+                    const int64_t* row_start, const pa_dims_t* dims, int64_t* rows_out,
+                    hipStream_t stream) {
+  if (dims == nullptr) return PA_EINVAL;
+  if (dims->num_seqs < 0 || dims->max_context_len < 0 || dims->max_pages_per_seq < 0)
+    return PA_EINVAL;
+  if (dims->page_size != 16) return PA_ENOTSUP;
+  if ((dims->max_context_len + 15) / 16 > dims->max_pages_per_seq) return PA_EINVAL;
+  if (dims->num_seqs == 0 || dims->max_context_len == 0) return PA_OK;
+  if (!block_table || !context_lens || !row_start || !rows_out) return PA_EINVAL;
+  hipError_t e = pa::launch_gather_trace(block_table, dims->max_pages_per_seq, context_lens, row_start,
+                                         dims->num_seqs, dims->max_context_len, rows_out, stream);
+  return e == hipSuccess ? PA_OK : PA_EHIP;
+}
+
+const char* pa_strerror(int code) {
+  switch (code) {
+    case PA_OK: return "success";
+    case PA_EINVAL: return "invalid argument (null pointer, negative or inconsistent size)";
+    case PA_ENOTSUP: return "unsupported configuration (head_dim, page_size, dtype or GQA group size)";
+    case PA_ENOSPC: return "workspace smaller than pa_workspace_size()";
+    case PA_EHIP: return "HIP kernel launch failed";
+    default: return "unknown error code";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,58 @@
+// Host-side launchers of the gfx950 kernels (internal to libpagedattn.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pa {
+
+// Arguments of the split-K attention kernel.  Flat grid of
+// n_split_slots * H_kv * rows workgroups; workgroup id = (row * H_kv + g) *
+// n_split_slots + split attends the s = H_q / H_kv query heads of KV head g
+// for query row `row` over pages [split * pages_per_split, +pages_per_split)
+// of the keys that row may see.  Decode: row = sequence.  Varlen: the row's
+// sequence is found in query_start_loc and its causal limit applied.
+struct DecodeArgs {
+  const void* q;             // [rows][H_q][D]
+  const void* k_pages;       // [num_pages][H_kv][16][D]
+  const void* v_pages;
+  const int32_t* block_table;
+  const int32_t* context_lens;
+  const int32_t* query_start_loc;  // [B+1] for varlen, nullptr for decode
+  void* out;                 // [rows][H_q][D]
+  float* ws_o;               // [rows][H_q][n_split_slots][D] partial outputs (unnormalised)
+  float* ws_ml;              // [rows][H_q][n_split_slots][2] (running max in log2 units, sum)
+  int64_t bt_stride;         // max_pages_per_seq
+  float scale_log2;          // scale * log2(e)
+  int B;                     // sequences
+  int max_context_len;       // declared bound; longer contexts are flagged
+  int H_q, H_kv;
+  int pages_per_split;
+  int n_split_slots;
+};
+
+struct ReduceArgs {
+  const float* ws_o;
+  const float* ws_ml;
+  const int32_t* context_lens;
+  const int32_t* query_start_loc;  // nullptr for decode
+  void* out;
+  int B, rows, H_q;
+  int max_context_len;
+  int pages_per_split;
+  int n_split_slots;
+};
+
+// dtype: 0 bf16, 1 fp32.  Return hipSuccess or the launch error.
+hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st);
+hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st);
+hipError_t launch_gather_trace(const int32_t* block_table, int64_t bt_stride,
+                               const int32_t* context_lens, const int64_t* row_start, int B,
+                               int max_context_len, int64_t* rows_out, hipStream_t st);
+
+// Maximum pages a workgroup's split may span (block-table entries are held one
+// per lane of each wave).
+constexpr int kDecodeWaves = 4;
+constexpr int kMaxPagesPerSplit = 64 * kDecodeWaves;
+
+}  // namespace pa

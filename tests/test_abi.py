@@ -1,0 +1,198 @@
+"""C ABI of libpagedattn.so on the host: the library loads, exports every entry
+point the header declares, and its host-side validation and workspace
+planning return the documented codes.  Validation runs before any HIP call,
+so the rejected calls below enqueue nothing; they use placeholder addresses
+and therefore run only where no GPU is visible (on a GPU the parity tests
+exercise the same paths with real buffers)."""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2504_09345_amd import binding as pb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pagedattn.h")
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+host_only = pytest.mark.skipif(_gpu_visible(), reason="placeholder addresses: host-only check")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:int|const char \*)\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    assert _declared() == sorted(pb.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pb.load()
+    for name in _declared():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", pb.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    syms = {l.split()[-1] for l in out.splitlines() if l.strip()}
+    for name in _declared():
+        assert name in syms, name
+
+
+def test_library_is_gfx950_only():
+    # the offload bundle of our own build names its code-object targets
+    blob = open(pb.LIB_PATH, "rb").read()
+    targets = set(re.findall(rb"amdgcn-amd-amdhsa-+(gfx[0-9a-z]+)", blob))
+    assert targets == {b"gfx950"}
+
+
+def test_strerror():
+    for code in (0, -1, -2, -3, -4):
+        assert len(pb.pa_strerror(code)) > 5
+    assert pb.pa_strerror(-99) == "unknown error code"
+    assert "workspace" in pb.pa_strerror(pb.PA_ENOSPC)
+
+
+def dims(**kw):
+    base = dict(num_seqs=256, num_q_heads=32, num_kv_heads=8, head_dim=128, page_size=16,
+                num_pages=25600, max_pages_per_seq=128, max_context_len=2048, pages_per_split=0,
+                dtype=pb.PA_BF16, num_q_rows=0, max_q_len=0)
+    base.update(kw)
+    return pb.PaDims(**base)
+
+
+def test_workspace_size_formula():
+    # default granule 32 pages: 2048 tokens = 128 pages = 4 splits
+    n = pb.pa_workspace_size(dims())
+    items = 256 * 32 * 4
+    align = lambda x: (x + 255) // 256 * 256
+    assert n == align(items * 128 * 4) + align(items * 2 * 4)
+    # one split: no workspace
+    assert pb.pa_workspace_size(dims(max_context_len=512)) == 0
+    assert pb.pa_workspace_size(dims(max_context_len=512, pages_per_split=8)) > 0
+    # varlen rows size the workspace
+    v = pb.pa_workspace_size(dims(num_q_rows=4608, max_q_len=512, num_seqs=520,
+                                  max_context_len=4096, max_pages_per_seq=256))
+    assert v == align(4608 * 32 * 8 * 128 * 4) + align(4608 * 32 * 8 * 2 * 4)
+    assert pb.pa_workspace_size(dims(num_seqs=0)) >= 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(num_q_heads=30), pb.PA_EINVAL),           # H_q not a multiple of H_kv
+    (dict(num_seqs=-1), pb.PA_EINVAL),
+    (dict(num_kv_heads=0), pb.PA_EINVAL),
+    (dict(head_dim=96), pb.PA_ENOTSUP),
+    (dict(page_size=32), pb.PA_ENOTSUP),
+    (dict(dtype=7), pb.PA_ENOTSUP),
+    (dict(num_q_heads=24, num_kv_heads=8), pb.PA_ENOTSUP),  # group of 3
+    (dict(max_pages_per_seq=100), pb.PA_EINVAL),    # row too short for max_context_len
+    (dict(max_context_len=-5), pb.PA_EINVAL),
+    (dict(pages_per_split=10000), pb.PA_EINVAL),
+    (dict(pages_per_split=-1), pb.PA_EINVAL),
+])
+def test_workspace_size_rejects(kw, code):
+    with pytest.raises(pb.PagedAttnError) as e:
+        pb.pa_workspace_size(dims(**kw))
+    assert e.value.code == code
+
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+@host_only
+@pytest.mark.parametrize("case", ["null_q", "null_out", "bad_group", "small_ws", "no_ws",
+                                  "nan_scale", "decode_rows", "decode_qlen", "hd"])
+def test_paged_attn_validation(case):
+    d = dims()
+    args = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, cl=FAKE, scale=0.088, out=FAKE, ws=FAKE,
+                ws_bytes=pb.pa_workspace_size(d))
+    expect = pb.PA_EINVAL
+    if case == "null_q":
+        args["q"] = None
+    elif case == "null_out":
+        args["out"] = None
+    elif case == "bad_group":
+        d.num_q_heads = 20
+    elif case == "small_ws":
+        args["ws_bytes"] -= 1
+        expect = pb.PA_ENOSPC
+    elif case == "no_ws":
+        args["ws"] = None
+        expect = pb.PA_ENOSPC
+    elif case == "nan_scale":
+        args["scale"] = float("nan")
+    elif case == "decode_rows":
+        d.num_q_rows = 7
+    elif case == "decode_qlen":
+        d.max_q_len = 3
+    elif case == "hd":
+        d.head_dim = 256
+        expect = pb.PA_ENOTSUP
+    lib = pb.load()
+    import ctypes
+    rc = lib.paged_attn(args["q"], args["k"], args["v"], args["bt"], args["cl"], args["scale"],
+                        args["out"], ctypes.byref(d), args["ws"], args["ws_bytes"], None, None)
+    assert rc == expect
+
+
+@host_only
+@pytest.mark.parametrize("case", ["null_qsl", "rows_without_qlen", "qlen_over_ctx", "small_ws"])
+def test_paged_attn_varlen_validation(case):
+    import ctypes
+    d = dims(num_seqs=520, num_q_rows=4608, max_q_len=512, max_context_len=4096,
+             max_pages_per_seq=256)
+    qsl, ws_bytes, expect = FAKE, pb.pa_workspace_size(d), pb.PA_EINVAL
+    if case == "null_qsl":
+        qsl = None
+    elif case == "rows_without_qlen":
+        d.max_q_len = 0
+        ws_bytes = 1 << 40
+    elif case == "qlen_over_ctx":
+        d.max_q_len = 5000
+        ws_bytes = 1 << 40
+    elif case == "small_ws":
+        ws_bytes -= 256
+        expect = pb.PA_ENOSPC
+    rc = pb.load().paged_attn_varlen(FAKE, FAKE, FAKE, FAKE, FAKE, qsl, 0.088, FAKE,
+                                     ctypes.byref(d), FAKE, ws_bytes, None, None)
+    assert rc == expect
+
+
+@host_only
+def test_gather_trace_validation():
+    import ctypes
+    lib = pb.load()
+    d = dims()
+    assert lib.pa_gather_trace(None, FAKE, FAKE, ctypes.byref(d), FAKE, None) == pb.PA_EINVAL
+    d2 = dims(page_size=8)
+    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, ctypes.byref(d2), FAKE, None) == pb.PA_ENOTSUP
+    d3 = dims(max_pages_per_seq=3)
+    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, ctypes.byref(d3), FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, None, FAKE, None) == pb.PA_EINVAL
+    # nothing to trace: success without touching the pointers
+    d4 = dims(num_seqs=0)
+    assert lib.pa_gather_trace(None, None, None, ctypes.byref(d4), None, None) == pb.PA_OK
+
+
+@host_only
+def test_empty_batch_is_a_no_op():
+    import ctypes
+    d = dims(num_seqs=0, max_context_len=0)
+    assert pb.load().paged_attn(None, None, None, None, None, 1.0, None, ctypes.byref(d), None, 0,
+                                None, None) == pb.PA_OK
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(pb, "_lib", None)
+    monkeypatch.setattr(pb, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        pb.load()

@@ -1,0 +1,206 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the
+same seeded inputs, element by element, plus the structural checks (bit-exact
+block-table gather, split-size invariance, determinism, poisoned pools, edge
+cases).  Full-size workloads are checked on sampled sequences in the launch
+configuration the benchmark times."""
+import functools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_09345_amd import binding as pb
+from paper_2504_09345_amd import workloads as W
+from parity_util import (announce, assert_parity, parity_stats, run_gpu, run_oracle, sub_batch,
+                         upload)
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    return torch
+
+
+# --- tiny and small shapes -------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("pps", [0, 1, 3])
+def test_tiny_decode(dtype, pps):
+    announce(f"tiny decode dtype={dtype} pages_per_split={pps}")
+    b = W.generate("tiny", seed=0, dtype=dtype)
+    got = run_gpu(b, pages_per_split=pps)
+    assert_parity(got, run_oracle(b), what=f"tiny {dtype} pps={pps}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_tiny_poisoned_pool(dtype):
+    announce(f"tiny poison dtype={dtype}")
+    b = W.generate("tiny", seed=1, dtype=dtype, poison=True)
+    for pps in (0, 2):
+        got = run_gpu(b, pages_per_split=pps)
+        assert_parity(got, run_oracle(b), what=f"poison pps={pps}")
+
+
+def test_fp32_inputs_match_tightly():
+    # with fp32 inputs and output only accumulation order differs
+    announce("tiny fp32 tight")
+    b = W.generate("tiny", seed=2, dtype="fp32")
+    st = parity_stats(run_gpu(b), run_oracle(b))
+    assert st["max_rel_global"] < 2e-5, st
+
+
+@pytest.mark.parametrize("s", [1, 2, 4, 6, 8])
+@pytest.mark.parametrize("D", [64, 128])
+def test_group_sizes_and_head_dims(s, D):
+    announce(f"edge contexts s={s} D={D}")
+    ctx = [1, 2, 15, 16, 17, 31, 32, 33, 100, 255, 256, 257, 511, 512, 513, 1000]
+    b = W.generate("tiny", seed=3 + s, overrides=dict(H_q=2 * s, H_kv=2, D=D,
+                                                      ctx=("list", ctx), pool=("factor", 1.5)))
+    ref = run_oracle(b)
+    for pps in (0, 1, 5):
+        assert_parity(run_gpu(b, pages_per_split=pps), ref, what=f"s={s} D={D} pps={pps}")
+
+
+def test_split_size_invariance():
+    announce("split invariance fp32 long contexts")
+    b = W.generate("tiny", seed=7, dtype="fp32",
+                   overrides=dict(ctx=("list", [3000, 777, 4096, 1, 2049]), pool=("factor", 1.3)))
+    outs = {pps: run_gpu(b, pages_per_split=pps) for pps in (1, 3, 32, 256)}
+    base = outs[256]
+    scale = np.abs(base).max()
+    for pps, o in outs.items():
+        assert np.abs(o - base).max() <= 1e-5 * scale, pps
+    assert_parity(base, run_oracle(b))
+
+
+def test_one_token_context_returns_v_exactly():
+    torch = _torch()
+    for dtype in ("bf16", "fp32"):
+        announce(f"ctx=1 exact dtype={dtype}")
+        b = W.generate("tiny", seed=8, dtype=dtype)
+        b.context_lens[:] = 1
+        got = run_gpu(b, max_context_len=200)
+        s = b.num_q_heads // b.num_kv_heads
+        for i in range(b.num_seqs):
+            page = b.block_table[i, 0]
+            for h in range(b.num_q_heads):
+                v0 = b.v_pages[page, h // s, 0]
+                v0 = W.bf16_bits_to_f32(v0) if dtype == "bf16" else v0
+                assert np.array_equal(got[i, h], v0)
+
+
+def test_empty_context_gives_zeros_and_determinism():
+    announce("ctx=0 zeros, determinism")
+    b = W.generate("tiny", seed=9)
+    b.context_lens[2] = 0
+    a1 = run_gpu(b, pages_per_split=2, max_context_len=200)
+    a2 = run_gpu(b, pages_per_split=2, max_context_len=200)
+    assert np.all(a1[2] == 0)
+    assert np.array_equal(a1.view(np.uint32), a2.view(np.uint32))
+    assert_parity(a1, run_oracle(b))
+
+
+def test_batch_independence():
+    announce("batch independence")
+    b = W.generate("tiny", seed=10, overrides=dict(ctx=("list", [50, 300, 7, 1024])))
+    full = run_gpu(b, max_context_len=1024)
+    for i in range(b.num_seqs):
+        sb, _ = sub_batch(b, [i])
+        alone = run_gpu(sb, max_context_len=1024)
+        assert np.array_equal(alone[0].view(np.uint32), full[i].view(np.uint32))
+
+
+def test_context_beyond_declared_bound_is_flagged():
+    # a context longer than max_context_len breaks the contract: the library
+    # reports NaN for that sequence instead of reading past the block-table row
+    announce("contract violation -> NaN")
+    b = W.generate("tiny", seed=11)
+    got = run_gpu(b, max_context_len=150)  # ctx 200 > 150 (table row holds 13 pages)
+    assert np.isnan(got[3]).all()
+    assert_parity(got[:3], run_oracle(b)[:3])
+
+
+def test_gather_trace_bit_exact():
+    torch = _torch()
+    for name, seed in (("tiny", 0), ("mixtral-256", 1)):
+        announce(f"gather trace {name}")
+        b = W.generate(name, seed=seed) if name == "tiny" else _full(name, seed)
+        bt = torch.from_numpy(b.block_table).cuda()
+        cl = torch.from_numpy(b.context_lens).cuda()
+        starts = np.zeros(b.num_seqs, np.int64)
+        starts[1:] = np.cumsum(b.context_lens.astype(np.int64))[:-1]
+        rs = torch.from_numpy(starts).cuda()
+        total = int(b.context_lens.sum())
+        rows = torch.full((total,), -7, dtype=torch.int64, device="cuda")
+        dims = pb.PaDims(num_seqs=b.num_seqs, num_q_heads=1, num_kv_heads=1, head_dim=128,
+                         page_size=16, num_pages=b.num_pages, max_pages_per_seq=b.max_pages_per_seq,
+                         max_context_len=int(b.context_lens.max()), pages_per_split=0, dtype=0,
+                         num_q_rows=0, max_q_len=0)
+        pb.pa_gather_trace(bt, cl, rs, dims, rows)
+        torch.cuda.synchronize()
+        ref = oracle.gather_indices(b.block_table, b.context_lens, 16, b.num_pages)
+        assert np.array_equal(rows.cpu().numpy(), ref)
+
+
+# --- varlen: causal prefill chunks sharing the launch with decode rows ------
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_varlen_small(dtype):
+    announce(f"varlen small dtype={dtype}")
+    b = W.generate("mixed", seed=3, dtype=dtype,
+                   overrides=dict(prefill=(3, 40, 0, 70), decode=(6, 1, 300), pool=("factor", 1.5)))
+    ref = run_oracle(b)
+    for pps in (0, 1, 4):
+        assert_parity(run_gpu(b, pages_per_split=pps), ref, strict=False, what=f"pps={pps}")
+
+
+def test_varlen_single_rows_equal_decode():
+    announce("varlen L=1 equals decode")
+    b = W.generate("tiny", seed=12, overrides=dict(ctx=("list", [33, 100, 1, 640])))
+    dec = run_gpu(b)
+    vb = W.Batch(**{**b.__dict__, "query_start_loc": np.arange(b.num_seqs + 1, dtype=np.int32)})
+    var = run_gpu(vb)
+    assert np.array_equal(dec.view(np.uint32), var.view(np.uint32))
+
+
+# --- full-size workloads, sampled -----------------------------------------
+
+@functools.lru_cache(maxsize=1)
+def _full(name, seed):
+    return W.generate(name, seed=seed)
+
+
+def _sample(batch, n, seed):
+    rng = np.random.default_rng(seed)
+    B = batch.num_seqs
+    pick = set(rng.choice(B, size=min(n, B), replace=False).tolist())
+    lens = batch.context_lens
+    pick |= {int(np.argmax(lens)), int(np.argmin(lens)), 0, B - 1}
+    return sorted(pick)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,seed,n", [("mixtral-256", 1, 48), ("long-ctx-64", 2, 6),
+                                         ("dbrx-512", 3, 48)])
+def test_full_size_decode_sampled(name, seed, n):
+    announce(f"full {name} seed={seed}: generate")
+    b = _full(name, seed)
+    announce(f"full {name}: gpu run B={b.num_seqs} max_ctx={int(b.context_lens.max())}")
+    got = run_gpu(b)
+    seqs = _sample(b, n, seed)
+    sb, rows = sub_batch(b, seqs)
+    ref = run_oracle(sb)
+    assert_parity(got[rows], ref, what=name)
+
+
+@pytest.mark.slow
+def test_full_size_mixed_sampled():
+    announce("full mixed seed=4: generate")
+    b = _full("mixed", 4)
+    announce(f"full mixed: gpu run rows={b.num_q_rows}")
+    got = run_gpu(b)
+    seqs = [0, 5] + list(range(8, 520, 16))
+    sb, rows = sub_batch(b, seqs)
+    ref = run_oracle(sb)
+    assert_parity(got[rows], ref, strict=False, what="mixed")
