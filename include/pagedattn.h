@@ -90,7 +90,9 @@ typedef struct pa_dims {
   int32_t num_pages;         /* pages in the pool                           */
   int32_t max_pages_per_seq; /* block_table row stride, >= ceil(max_context_len / 16) */
   int32_t max_context_len;   /* upper bound on context_lens[], sizes the grid */
-  int32_t pages_per_split;   /* split-K granule in pages; 0 = library default */
+  int32_t pages_per_split;   /* 0: library choice (persistent stream-K kernel
+                                where the batch fits it); > 0: per-row split-K
+                                kernel with this many pages per workgroup      */
   int32_t dtype;             /* pa_dtype_t                                  */
   int32_t num_q_rows;        /* varlen: total query rows; decode: 0 or num_seqs */
   int32_t max_q_len;         /* varlen: bound on any chunk length; decode: 0 or 1 */

@@ -12,7 +12,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "_lib", "libpagedattn.so")
+# PAGEDATTN_LIB selects another build of the same library (e.g. one compiled
+# with different tuning macros); default: the in-tree build.
+LIB_PATH = os.environ.get("PAGEDATTN_LIB") or os.path.join(HERE, "_lib", "libpagedattn.so")
 
 PA_OK, PA_EINVAL, PA_ENOTSUP, PA_ENOSPC, PA_EHIP = 0, -1, -2, -3, -4
 PA_BF16, PA_FP32 = 0, 1

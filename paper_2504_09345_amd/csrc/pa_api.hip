@@ -11,17 +11,24 @@
 
 namespace {
 
-// Default split-K granule: 32 pages = 512 tokens per workgroup (8 pages per
-// wave).  Long contexts get many splits; short ones run unsplit.
-constexpr int kDefaultPagesPerSplit = 32;
+// Split-K granule of the per-row path when the caller leaves it to the
+// library: 128 pages = 2048 tokens per workgroup (32 pages per wave).
+constexpr int kDefaultPagesPerSplit = 128;
 
 struct Plan {
   int s = 0;
+  int rows = 0;
+  // stream-K path (decode rows)
+  bool stream = false;
+  int W = 0, nb = 0;
+  int64_t g_min = 0;  // persistent workgroups needed to keep every range within the LDS unit table
+  size_t st_o = 0, st_ml = 0, st_cum = 0;
+  // split-K path (all rows of a decode call that the stream path cannot take,
+  // or the chunked-prefill rows of a varlen call)
+  bool split = false;
   int pps = 0;
   int n_split_slots = 0;
-  int rows = 0;
-  size_t ws_o_bytes = 0;
-  size_t ws_ml_bytes = 0;
+  size_t sp_o = 0, sp_ml = 0;
   size_t ws_bytes = 0;
 };
 
@@ -55,17 +62,42 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
     rows = d->num_seqs;
   }
   p->s = s;
+  p->rows = rows;
+
+  // stream-K: W = widest power of two <= 8 dividing H_kv waves per workgroup
+  p->W = (d->num_kv_heads % 8 == 0 && pa::kStreamMaxWaves >= 8) ? 8
+         : (d->num_kv_heads % 4 == 0 && pa::kStreamMaxWaves >= 4) ? 4
+         : (d->num_kv_heads % 2 == 0 && pa::kStreamMaxWaves >= 2) ? 2 : 1;
+  p->nb = d->num_kv_heads / p->W;
+  const int64_t u_max = (int64_t)p->nb * d->num_seqs * max_pages;
+  p->g_min = (u_max + pa::kStreamMaxUnits - 1) / pa::kStreamMaxUnits;
+  // an explicit split granule asks for the split-K path
+  p->stream = d->pages_per_split == 0 && d->num_seqs <= pa::kStreamMaxRows && p->nb < 64 &&
+              rows < (1 << 19) && p->g_min <= pa::kStreamMaxGrid;
+  if (p->stream) {
+    const size_t recs = (size_t)pa::kStreamMaxGrid * 2 * p->W * s;  // (workgroup, slot, wave, head)
+    p->st_o = align256(recs * (size_t)d->head_dim * sizeof(float));
+    p->st_ml = align256(recs * 2 * sizeof(float));
+    p->st_cum = align256(((size_t)d->num_seqs + 1) * sizeof(int32_t));
+  }
+  // split-K for whatever the stream path does not take
+  p->split = varlen ? rows > 0 : !p->stream;
   p->pps = d->pages_per_split > 0 ? d->pages_per_split : kDefaultPagesPerSplit;
   p->n_split_slots = (int)((max_pages + p->pps - 1) / p->pps);
   if (p->n_split_slots < 1) p->n_split_slots = 1;
-  p->rows = rows;
-  if ((int64_t)rows * d->num_kv_heads * p->n_split_slots > 0x7fffffffLL) return PA_ENOTSUP;
-  if (p->n_split_slots > 1) {
-    const size_t items = (size_t)rows * (size_t)d->num_q_heads * (size_t)p->n_split_slots;
-    p->ws_o_bytes = align256(items * (size_t)d->head_dim * sizeof(float));
-    p->ws_ml_bytes = align256(items * 2 * sizeof(float));
+  if (p->split) {
+    if ((int64_t)rows * d->num_kv_heads * p->n_split_slots > 0x7fffffffLL) return PA_ENOTSUP;
+    if (p->n_split_slots > 1) {
+      const size_t items = (size_t)rows * (size_t)d->num_q_heads * (size_t)p->n_split_slots;
+      p->sp_o = align256(items * (size_t)d->head_dim * sizeof(float));
+      p->sp_ml = align256(items * 2 * sizeof(float));
+    }
   }
-  p->ws_bytes = p->ws_o_bytes + p->ws_ml_bytes;
+  if (rows == 0) {  // nothing to launch, nothing to hold
+    p->stream = p->split = false;
+    p->st_o = p->st_ml = p->st_cum = p->sp_o = p->sp_ml = 0;
+  }
+  p->ws_bytes = p->st_o + p->st_ml + p->st_cum + p->sp_o + p->sp_ml;
   return PA_OK;
 }
 
@@ -86,6 +118,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     if (varlen && !query_start_loc) return PA_EINVAL;
   }
   if (p.ws_bytes > 0 && (workspace == nullptr || workspace_bytes < p.ws_bytes)) return PA_ENOSPC;
+  if (p.rows > 0 && p.split == false && p.stream == false) return PA_ENOTSUP;
 
   const hipEvent_t ev_begin = timing ? timing->attn_begin : nullptr;
   const hipEvent_t ev_attn = timing ? timing->attn_end : nullptr;
@@ -97,31 +130,75 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     return PA_OK;
   }
 
-  pa::DecodeArgs a;
-  a.q = q;
-  a.k_pages = k_pages;
-  a.v_pages = v_pages;
-  a.block_table = block_table;
-  a.context_lens = context_lens;
-  a.query_start_loc = varlen ? query_start_loc : nullptr;
-  a.out = out;
-  a.ws_o = p.ws_bytes ? static_cast<float*>(workspace) : nullptr;
-  a.ws_ml = p.ws_bytes ? reinterpret_cast<float*>(static_cast<char*>(workspace) + p.ws_o_bytes) : nullptr;
-  a.bt_stride = dims->max_pages_per_seq;
-  a.scale_log2 = scale * 1.4426950408889634f;
-  a.B = dims->num_seqs;
-  a.max_context_len = dims->max_context_len;
-  a.H_q = dims->num_q_heads;
-  a.H_kv = dims->num_kv_heads;
-  a.pages_per_split = p.pps;
-  a.n_split_slots = p.n_split_slots;
-
+  char* ws = static_cast<char*>(workspace);
   record(ev_begin, stream);
-  hipError_t e = pa::launch_decode(dims->dtype, dims->head_dim, p.s, a, p.rows, stream);
-  if (e != hipSuccess) return PA_EHIP;
+  hipError_t e = hipSuccess;
+  pa::StreamArgs sa{};
+  int G = 0;
+  if (p.stream) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return PA_EHIP;
+    const int per_cu = pa::stream_occupancy(dims->dtype, dims->head_dim, p.s, p.W);
+    if (per_cu <= 0) return PA_EHIP;
+    int64_t g = (int64_t)per_cu * cus;
+    if (g < p.g_min) g = p.g_min;
+    if (g > pa::kStreamMaxGrid) g = pa::kStreamMaxGrid;
+    G = (int)g;
+    sa.q = q;
+    sa.k_pages = k_pages;
+    sa.v_pages = v_pages;
+    sa.block_table = block_table;
+    sa.context_lens = context_lens;
+    sa.query_start_loc = varlen ? query_start_loc : nullptr;
+    sa.out = out;
+    sa.ws_o = reinterpret_cast<float*>(ws);
+    sa.ws_ml = reinterpret_cast<float*>(ws + p.st_o);
+    sa.ws_cum = reinterpret_cast<int32_t*>(ws + p.st_o + p.st_ml);
+    sa.bt_stride = dims->max_pages_per_seq;
+    sa.scale_log2 = scale * 1.4426950408889634f;
+    sa.B = dims->num_seqs;
+    sa.H_q = dims->num_q_heads;
+    sa.H_kv = dims->num_kv_heads;
+    sa.max_context_len = dims->max_context_len;
+    sa.nb = p.nb;
+    if (sa.B > 0) {
+      e = pa::launch_stream(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream);
+      if (e != hipSuccess) return PA_EHIP;
+    }
+  }
+  pa::DecodeArgs a{};
+  if (p.split) {
+    char* sp = ws + p.st_o + p.st_ml + p.st_cum;
+    a.q = q;
+    a.k_pages = k_pages;
+    a.v_pages = v_pages;
+    a.block_table = block_table;
+    a.context_lens = context_lens;
+    a.query_start_loc = varlen ? query_start_loc : nullptr;
+    a.out = out;
+    a.ws_o = p.sp_o ? reinterpret_cast<float*>(sp) : nullptr;
+    a.ws_ml = p.sp_o ? reinterpret_cast<float*>(sp + p.sp_o) : nullptr;
+    a.bt_stride = dims->max_pages_per_seq;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.B = dims->num_seqs;
+    a.max_context_len = dims->max_context_len;
+    a.H_q = dims->num_q_heads;
+    a.H_kv = dims->num_kv_heads;
+    a.pages_per_split = p.pps;
+    a.n_split_slots = p.n_split_slots;
+    a.skip_single_rows = p.stream ? 1 : 0;
+    e = pa::launch_decode(dims->dtype, dims->head_dim, p.s, a, p.rows, stream);
+    if (e != hipSuccess) return PA_EHIP;
+  }
   record(ev_attn, stream);
-  if (p.n_split_slots > 1) {
-    pa::ReduceArgs r;
+  if (p.stream && sa.B > 0) {
+    e = pa::launch_stream_fixup(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream);
+    if (e != hipSuccess) return PA_EHIP;
+  }
+  if (p.split && p.n_split_slots > 1) {
+    pa::ReduceArgs r{};
     r.ws_o = a.ws_o;
     r.ws_ml = a.ws_ml;
     r.context_lens = context_lens;
@@ -133,6 +210,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     r.max_context_len = dims->max_context_len;
     r.pages_per_split = p.pps;
     r.n_split_slots = p.n_split_slots;
+    r.skip_single_rows = a.skip_single_rows;
     e = pa::launch_reduce(dims->dtype, dims->head_dim, r, stream);
     if (e != hipSuccess) return PA_EHIP;
   }

@@ -27,156 +27,11 @@
 // kernel merges the splits.
 #include "pa_device.h"
 #include "pa_kernels.h"
+#include "pa_tile.h"
 
 namespace pa {
 
-template <typename T, int D, int S>
-struct DecodeShape {
-  static constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16-byte lane load
-  static constexpr int LPT = D / VEC;              // lanes per token row
-  static constexpr int TPI = 64 / LPT;             // token rows per wave-wide load
-  static constexpr int NI = kPage / TPI;           // loads per 16-token tile
-  static_assert(LPT >= 2 && LPT <= 32 && 64 % LPT == 0 && kPage % TPI == 0, "unsupported shape");
-};
-
-// Partial dot product of the lane's VEC query elements with VEC key elements.
-__device__ __forceinline__ float lane_dot(const u32x4& q, const u32x4& k, uint16_t) {
-  float acc = 0.0f;
-  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.x), as_bf16x2(k.x), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.y), as_bf16x2(k.y), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.z), as_bf16x2(k.z), acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.w), as_bf16x2(k.w), acc, false);
-  return acc;
-}
-__device__ __forceinline__ float lane_dot(const u32x4& q, const u32x4& k, float) {
-  float acc = __uint_as_float(q.x) * __uint_as_float(k.x);
-  acc = fmaf(__uint_as_float(q.y), __uint_as_float(k.y), acc);
-  acc = fmaf(__uint_as_float(q.z), __uint_as_float(k.z), acc);
-  acc = fmaf(__uint_as_float(q.w), __uint_as_float(k.w), acc);
-  return acc;
-}
-
-// Widen the lane's VEC value elements to fp32.
-__device__ __forceinline__ void widen(const u32x4& v, float* f, uint16_t) {
-  f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x);
-  f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
-  f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z);
-  f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
-}
-__device__ __forceinline__ void widen(const u32x4& v, float* f, float) {
-  f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
-  f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
-}
-
-template <typename T, int D, int S>
-struct DecodeState {
-  using Sh = DecodeShape<T, D, S>;
-  u32x4 q[S];                  // lane's slice of the s query vectors (raw)
-  float o[S][Sh::VEC];         // unnormalised output slice per head
-  float m[S], l[S];            // running max (log2 units) and sum per head
-};
-
-// One (page, g) tile: NI K loads and NI V loads per lane.
-template <typename T, int D, int S>
-__device__ __forceinline__ void load_tile(const T* __restrict__ kp, const T* __restrict__ vp,
-                                          int64_t tile, int lane, u32x4 (&k)[DecodeShape<T, D, S>::NI],
-                                          u32x4 (&v)[DecodeShape<T, D, S>::NI]) {
-  using Sh = DecodeShape<T, D, S>;
-  const u32x4* kt = reinterpret_cast<const u32x4*>(kp + tile) + lane;
-  const u32x4* vt = reinterpret_cast<const u32x4*>(vp + tile) + lane;
-#pragma unroll
-  for (int i = 0; i < Sh::NI; ++i) k[i] = __builtin_nontemporal_load(kt + 64 * i);
-#pragma unroll
-  for (int i = 0; i < Sh::NI; ++i) v[i] = __builtin_nontemporal_load(vt + 64 * i);
-}
-
-// Fold one tile into the running state.  MASKED: tokens at or past `ctx`
-// (only in a sequence's last page) get logit -inf and value 0, so whatever
-// bytes the unused slots hold (even NaN) cannot reach the result.
-template <typename T, int D, int S, bool MASKED>
-__device__ __forceinline__ void process_tile(DecodeState<T, D, S>& st,
-                                             const u32x4 (&k)[DecodeShape<T, D, S>::NI],
-                                             u32x4 (&v)[DecodeShape<T, D, S>::NI], int row,
-                                             int first_token, int ctx, float scale_log2) {
-  using Sh = DecodeShape<T, D, S>;
-  float x[S][Sh::NI];
-#pragma unroll
-  for (int i = 0; i < Sh::NI; ++i)
-#pragma unroll
-    for (int j = 0; j < S; ++j) x[j][i] = lane_dot(st.q[j], k[i], T());
-#pragma unroll
-  for (int i = 0; i < Sh::NI; ++i)
-#pragma unroll
-    for (int j = 0; j < S; ++j) x[j][i] = group_sum<Sh::LPT>(x[j][i]) * scale_log2;
-  if constexpr (MASKED) {
-#pragma unroll
-    for (int i = 0; i < Sh::NI; ++i) {
-      const bool dead = first_token + row + Sh::TPI * i >= ctx;
-#pragma unroll
-      for (int j = 0; j < S; ++j) x[j][i] = dead ? -INFINITY : x[j][i];
-      v[i].x = dead ? 0u : v[i].x;
-      v[i].y = dead ? 0u : v[i].y;
-      v[i].z = dead ? 0u : v[i].z;
-      v[i].w = dead ? 0u : v[i].w;
-    }
-  }
-  float vf[Sh::NI][Sh::VEC];
-#pragma unroll
-  for (int i = 0; i < Sh::NI; ++i) widen(v[i], vf[i], T());
-#pragma unroll
-  for (int j = 0; j < S; ++j) {
-    float mx = x[j][0];
-#pragma unroll
-    for (int i = 1; i < Sh::NI; ++i) mx = fmaxf(mx, x[j][i]);
-    const float mnew = fmaxf(st.m[j], mx);
-    const float alpha = fast_exp2(st.m[j] - mnew);
-    st.m[j] = mnew;
-    float p[Sh::NI];
-    float psum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < Sh::NI; ++i) {
-      p[i] = fast_exp2(x[j][i] - mnew);
-      psum += p[i];
-    }
-    st.l[j] = fmaf(st.l[j], alpha, psum);
-#pragma unroll
-    for (int e = 0; e < Sh::VEC; ++e) {
-      float acc = st.o[j][e] * alpha;
-#pragma unroll
-      for (int i = 0; i < Sh::NI; ++i) acc = fmaf(p[i], vf[i][e], acc);
-      st.o[j][e] = acc;
-    }
-  }
-}
-
-// Sequence b and visible-key count n_vis of query row `row`.  Decode: row = b
-// and all ctx keys are visible.  Varlen: b is the largest sequence with
-// query_start_loc[b] <= row, and row r of a chunk of length L sees keys
-// 0 .. ctx - L + r.  Returns false when the row breaks the call's contract
-// (negative length, a context above max_context_len, a chunk longer than its
-// context); such rows are written as NaN by the attention kernel and left
-// alone by the reduction.
-__device__ __forceinline__ bool row_context(const int32_t* __restrict__ qsl,
-                                            const int32_t* __restrict__ context_lens, int B,
-                                            int max_context_len, int row, int& b, int& n_vis) {
-  if (qsl == nullptr) {
-    b = row;
-    n_vis = context_lens[row];
-    return n_vis >= 0 && n_vis <= max_context_len;
-  }
-  int lo = 0, hi = B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (qsl[mid] <= row) lo = mid; else hi = mid - 1;
-  }
-  b = lo;
-  const int ctx = context_lens[b];
-  const int L = qsl[b + 1] - qsl[b];
-  n_vis = ctx - L + (row - qsl[b]) + 1;
-  return ctx >= 0 && ctx <= max_context_len && n_vis >= 1;
-}
-
-template <typename T, int D, int S, int WAVES>
+template <typename T, int D, int S, int WAVES, int NBUF>
 __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeArgs a) {
   using Sh = DecodeShape<T, D, S>;
   constexpr int NT = 64 * WAVES;
@@ -186,9 +41,11 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeArgs a) {
   const int split = blockIdx.x % a.n_split_slots;
   const int rest = blockIdx.x / a.n_split_slots;
   const int g = rest % a.H_kv, row_idx = rest / a.H_kv;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: keep it scalar
   int b, ctx;  // ctx: keys this row sees
   const bool ok = row_context(a.query_start_loc, a.context_lens, a.B, a.max_context_len, row_idx, b, ctx);
+  if (a.skip_single_rows && a.query_start_loc[b + 1] - a.query_start_loc[b] == 1) return;
   const int n_pages = ok ? (ctx + kPage - 1) / kPage : 0;
   const int pps = a.pages_per_split;
   const int p0 = split * pps;
@@ -230,31 +87,39 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeArgs a) {
 
   const T* kp = reinterpret_cast<const T*>(a.k_pages);
   const T* vp = reinterpret_cast<const T*>(a.v_pages);
-  const int last_page = n_pages - 1;
-  const bool ragged = (ctx % kPage) != 0;
+  const int lane_off = lane * 16;
 
-  auto tile_of = [&](int kk) {
-    const int32_t page = __builtin_amdgcn_readlane(bt_lane, kk);
-    return tile_offset(page, g, a.H_kv, D);
+  // Ring of NBUF register tile buffers: while tile k is folded, the loads of
+  // tiles k+1 .. k+NBUF-1 are in flight.  Loads are issued unconditionally;
+  // a tile index past the wave's pages gets a null descriptor (zeros, no
+  // memory access), so the number of outstanding loads is the same on every
+  // path and the wait before each fold is a fixed count.
+  auto issue = [&](u32x4 (&kr)[Sh::NI], u32x4 (&vr)[Sh::NI], int kk) {
+    int valid = 0;
+    int64_t off = 0;
+    if (kk < my_n) {
+      const int p = p0 + wave + WAVES * kk;
+      const int32_t page = __builtin_amdgcn_readlane(bt_lane, kk);
+      off = tile_offset(page, g, a.H_kv, D);
+      valid = min(kPage, ctx - p * kPage);
+    }
+    issue_tile<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), tile_rsrc<T, D>(vp + off, valid), lane_off, kr, vr);
   };
-  auto fold = [&](const u32x4 (&kr)[Sh::NI], u32x4 (&vr)[Sh::NI], int kk) {
-    const int p = p0 + wave + WAVES * kk;
-    if (ragged && p == last_page)
-      process_tile<T, D, S, true>(st, kr, vr, row, p * kPage, ctx, a.scale_log2);
-    else
-      process_tile<T, D, S, false>(st, kr, vr, row, p * kPage, ctx, a.scale_log2);
+  auto fold = [&](const u32x4 (&kr)[Sh::NI], const u32x4 (&vr)[Sh::NI], int kk) {
+    if (kk < my_n) {
+      const int p = p0 + wave + WAVES * kk;
+      fold_tile<T, D, S>(st, kr, vr, row, min(kPage, ctx - p * kPage), a.scale_log2);
+    }
   };
 
-  // Two register buffers: the next tile's loads are in flight while the
-  // current one is folded.
-  u32x4 kA[Sh::NI], vA[Sh::NI], kB[Sh::NI], vB[Sh::NI];
-  if (my_n > 0) load_tile<T, D, S>(kp, vp, tile_of(0), lane, kA, vA);
-  for (int kk = 0; kk < my_n; kk += 2) {
-    if (kk + 1 < my_n) load_tile<T, D, S>(kp, vp, tile_of(kk + 1), lane, kB, vB);
-    fold(kA, vA, kk);
-    if (kk + 1 < my_n) {
-      if (kk + 2 < my_n) load_tile<T, D, S>(kp, vp, tile_of(kk + 2), lane, kA, vA);
-      fold(kB, vB, kk + 1);
+  u32x4 kr[NBUF][Sh::NI], vr[NBUF][Sh::NI];
+#pragma unroll
+  for (int u = 0; u + 1 < NBUF; ++u) issue(kr[u], vr[u], u);
+  for (int base = 0; base < my_n; base += NBUF) {
+#pragma unroll
+    for (int u = 0; u < NBUF; ++u) {
+      issue(kr[(u + NBUF - 1) % NBUF], vr[(u + NBUF - 1) % NBUF], base + u + NBUF - 1);
+      fold(kr[u], vr[u], base + u);
     }
   }
 
@@ -313,6 +178,7 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
   if (item >= a.rows * a.H_q) return;
   int b, ctx;
   if (!row_context(a.query_start_loc, a.context_lens, a.B, a.max_context_len, item / a.H_q, b, ctx)) return;
+  if (a.skip_single_rows && a.query_start_loc[b + 1] - a.query_start_loc[b] == 1) return;
   const int n_pages = (ctx + kPage - 1) / kPage;
   const int n_splits = (n_pages + a.pages_per_split - 1) / a.pages_per_split;
   if (n_splits <= 1 || n_splits > a.n_split_slots) return;  // written by the attention kernel
@@ -356,11 +222,11 @@ static hipError_t decode_s(int s, const DecodeArgs& a, int rows, hipStream_t st)
   if (n > 0x7fffffffLL) return hipErrorInvalidConfiguration;
   const dim3 grid((unsigned)n), block(64 * kDecodeWaves);
   switch (s) {
-    case 1: decode_kernel<T, D, 1, kDecodeWaves><<<grid, block, 0, st>>>(a); break;
-    case 2: decode_kernel<T, D, 2, kDecodeWaves><<<grid, block, 0, st>>>(a); break;
-    case 4: decode_kernel<T, D, 4, kDecodeWaves><<<grid, block, 0, st>>>(a); break;
-    case 6: decode_kernel<T, D, 6, kDecodeWaves><<<grid, block, 0, st>>>(a); break;
-    case 8: decode_kernel<T, D, 8, kDecodeWaves><<<grid, block, 0, st>>>(a); break;
+    case 1: decode_kernel<T, D, 1, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
+    case 2: decode_kernel<T, D, 2, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
+    case 4: decode_kernel<T, D, 4, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
+    case 6: decode_kernel<T, D, 6, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
+    case 8: decode_kernel<T, D, 8, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -29,6 +29,7 @@ struct DecodeArgs {
   int H_q, H_kv;
   int pages_per_split;
   int n_split_slots;
+  int skip_single_rows;      // varlen: leave one-row sequences to the stream kernel
 };
 
 struct ReduceArgs {
@@ -41,7 +42,44 @@ struct ReduceArgs {
   int max_context_len;
   int pages_per_split;
   int n_split_slots;
+  int skip_single_rows;
 };
+
+// Arguments of the persistent stream-K kernel and its fixup.  Items are
+// (sequence, KV head); for varlen calls only sequences with exactly one
+// query row are taken (chunked prefill rows go to the per-row kernel).
+struct StreamArgs {
+  const void* q;
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* block_table;
+  const int32_t* context_lens;
+  const int32_t* query_start_loc;  // nullptr for decode
+  void* out;
+  float* ws_o;       // [G][2][W][s][D] partial outputs (slot 0 head, 1 tail)
+  float* ws_ml;      // [G][2][W][s][2]
+  int32_t* ws_cum;   // [B+1] page prefix sums, written by workgroup 0
+  int64_t bt_stride;
+  float scale_log2;
+  int B, H_q, H_kv, max_context_len;
+  int nb;            // head blocks = H_kv / W
+};
+
+constexpr int kStreamMaxRows = 8192;    // sequences per call on the stream path
+constexpr int kStreamMaxUnits = 2048;   // units per workgroup range (LDS unit table)
+constexpr int kStreamMaxGrid = 1024;    // persistent workgroups (partial-record space)
+#ifndef PA_STREAM_RING
+#define PA_STREAM_RING 2
+#endif
+constexpr int kStreamRing = PA_STREAM_RING;
+#ifndef PA_STREAM_MAX_WAVES
+#define PA_STREAM_MAX_WAVES 8
+#endif
+constexpr int kStreamMaxWaves = PA_STREAM_MAX_WAVES;  // waves (KV heads) per stream workgroup
+
+hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
+hipError_t launch_stream_fixup(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
+int stream_occupancy(int dtype, int D, int s, int W);  // workgroups per CU, 0 on error
 
 // dtype: 0 bf16, 1 fp32.  Return hipSuccess or the launch error.
 hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st);
@@ -52,7 +90,14 @@ hipError_t launch_gather_trace(const int32_t* block_table, int64_t bt_stride,
 
 // Maximum pages a workgroup's split may span (block-table entries are held one
 // per lane of each wave).
-constexpr int kDecodeWaves = 4;
+#ifndef PA_DECODE_WAVES
+#define PA_DECODE_WAVES 4
+#endif
+#ifndef PA_DECODE_RING
+#define PA_DECODE_RING 2
+#endif
+constexpr int kDecodeWaves = PA_DECODE_WAVES;  // waves per workgroup sharing one split
+constexpr int kDecodeRing = PA_DECODE_RING;    // register tile buffers per wave
 constexpr int kMaxPagesPerSplit = 64 * kDecodeWaves;
 
 }  // namespace pa

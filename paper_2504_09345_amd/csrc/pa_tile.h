@@ -1,0 +1,260 @@
+// Tile-level building blocks shared by the split-K and stream-K attention
+// kernels: the lane layout of a (page, KV head) tile, the bf16 dot products,
+// the buffer-descriptor loads, the online-softmax fold of one tile, the
+// merge of a wave's lane rows, and the mapping from a query row to its
+// sequence and visible keys.
+#pragma once
+
+#include "pa_device.h"
+
+namespace pa {
+
+template <typename T, int D, int S>
+struct DecodeShape {
+  static constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16-byte lane load
+  static constexpr int LPT = D / VEC;              // lanes per token row
+  static constexpr int TPI = 64 / LPT;             // token rows per wave-wide load
+  static constexpr int NI = kPage / TPI;           // loads per 16-token tile
+  static_assert(LPT >= 2 && LPT <= 32 && 64 % LPT == 0 && kPage % TPI == 0, "unsupported shape");
+};
+
+// Partial dot product of the lane's VEC query elements with VEC key elements.
+__device__ __forceinline__ float lane_dot(const u32x4& q, const u32x4& k, uint16_t) {
+  float acc = 0.0f;
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.x), as_bf16x2(k.x), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.y), as_bf16x2(k.y), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.z), as_bf16x2(k.z), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(q.w), as_bf16x2(k.w), acc, false);
+  return acc;
+}
+__device__ __forceinline__ float lane_dot(const u32x4& q, const u32x4& k, float) {
+  float acc = __uint_as_float(q.x) * __uint_as_float(k.x);
+  acc = fmaf(__uint_as_float(q.y), __uint_as_float(k.y), acc);
+  acc = fmaf(__uint_as_float(q.z), __uint_as_float(k.z), acc);
+  acc = fmaf(__uint_as_float(q.w), __uint_as_float(k.w), acc);
+  return acc;
+}
+
+// Widen the lane's VEC value elements to fp32.
+__device__ __forceinline__ void widen(const u32x4& v, float* f, uint16_t) {
+  f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x);
+  f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+  f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z);
+  f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
+}
+__device__ __forceinline__ void widen(const u32x4& v, float* f, float) {
+  f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+  f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+}
+
+template <typename T, int D, int S>
+struct DecodeState {
+  using Sh = DecodeShape<T, D, S>;
+  u32x4 q[S];                  // lane's slice of the s query vectors (raw)
+  float o[S][Sh::VEC];         // unnormalised output slice per head
+  float m[S], l[S];            // running max (log2 units) and sum per head
+};
+
+// Buffer descriptor (raw, untyped) of one (page, g) tile of `valid` tokens:
+// loads at byte offsets >= valid * D * sizeof(T) return zeros without a
+// memory access, so slots past the context (and whole null tiles, valid = 0)
+// never reach the arithmetic as anything but 0.
+template <typename T, int D>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const T* base, int valid) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), (short)0, valid * D * (int)sizeof(T),
+                                           0x00020000);
+}
+
+// Issue the NI K and NI V 16-byte-per-lane loads of one tile.  Lane l reads
+// bytes [16 l, 16 l + 16) of each 1 KiB slice: fully coalesced.
+template <int NI>
+__device__ __forceinline__ void issue_tile(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int lane_off,
+                                           u32x4 (&k)[NI], u32x4 (&v)[NI]) {
+#pragma unroll
+  for (int i = 0; i < NI; ++i) k[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off, i * 1024, 0);
+#pragma unroll
+  for (int i = 0; i < NI; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, lane_off, i * 1024, 0);
+}
+
+// Fold one tile into the running state.  `valid` (wave-uniform) is the number
+// of live tokens in the tile; tokens at or past it get logit -inf (their V
+// was already read as 0 by the buffer range check), so whatever bytes the
+// unused slots hold (even NaN) cannot reach the result.
+template <typename T, int D, int S>
+__device__ __forceinline__ void fold_tile(DecodeState<T, D, S>& st, const u32x4 (&k)[DecodeShape<T, D, S>::NI],
+                                          const u32x4 (&v)[DecodeShape<T, D, S>::NI], int row, int valid,
+                                          float scale_log2) {
+  using Sh = DecodeShape<T, D, S>;
+  float x[S][Sh::NI];
+#pragma unroll
+  for (int i = 0; i < Sh::NI; ++i)
+#pragma unroll
+    for (int j = 0; j < S; ++j) x[j][i] = lane_dot(st.q[j], k[i], T());
+#pragma unroll
+  for (int i = 0; i < Sh::NI; ++i)
+#pragma unroll
+    for (int j = 0; j < S; ++j) x[j][i] = group_sum<Sh::LPT>(x[j][i]) * scale_log2;
+  if (valid < kPage) {  // wave-uniform: only a sequence's last page
+#pragma unroll
+    for (int i = 0; i < Sh::NI; ++i) {
+      const bool dead = row + Sh::TPI * i >= valid;
+#pragma unroll
+      for (int j = 0; j < S; ++j) x[j][i] = dead ? -INFINITY : x[j][i];
+    }
+  }
+  float vf[Sh::NI][Sh::VEC];
+#pragma unroll
+  for (int i = 0; i < Sh::NI; ++i) widen(v[i], vf[i], T());
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    float mx = x[j][0];
+#pragma unroll
+    for (int i = 1; i < Sh::NI; ++i) mx = fmaxf(mx, x[j][i]);
+    const float mnew = fmaxf(st.m[j], mx);
+    const float alpha = fast_exp2(st.m[j] - mnew);
+    st.m[j] = mnew;
+    float p[Sh::NI];
+    float psum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < Sh::NI; ++i) {
+      p[i] = fast_exp2(x[j][i] - mnew);
+      psum += p[i];
+    }
+    st.l[j] = fmaf(st.l[j], alpha, psum);
+#pragma unroll
+    for (int e = 0; e < Sh::VEC; ++e) {
+      float acc = st.o[j][e] * alpha;
+#pragma unroll
+      for (int i = 0; i < Sh::NI; ++i) acc = fmaf(p[i], vf[i][e], acc);
+      st.o[j][e] = acc;
+    }
+  }
+}
+
+// Sequence b and visible-key count n_vis of query row `row`.  Decode: row = b
+// and all ctx keys are visible.  Varlen: b is the largest sequence with
+// query_start_loc[b] <= row, and row r of a chunk of length L sees keys
+// 0 .. ctx - L + r.  Returns false when the row breaks the call's contract
+// (negative length, a context above max_context_len, a chunk longer than its
+// context); such rows are written as NaN by the attention kernel and left
+// alone by the reduction.
+__device__ __forceinline__ bool row_context(const int32_t* __restrict__ qsl,
+                                            const int32_t* __restrict__ context_lens, int B,
+                                            int max_context_len, int row, int& b, int& n_vis) {
+  if (qsl == nullptr) {
+    b = row;
+    n_vis = context_lens[row];
+    return n_vis >= 0 && n_vis <= max_context_len;
+  }
+  int lo = 0, hi = B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (qsl[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  b = lo;
+  const int ctx = context_lens[b];
+  const int L = qsl[b + 1] - qsl[b];
+  n_vis = ctx - L + (row - qsl[b]) + 1;
+  return ctx >= 0 && ctx <= max_context_len && n_vis >= 1;
+}
+
+// Decode row of sequence b for the stream kernel.  Returns 1 (attend: q/out
+// row `row`, all nv cached keys visible), 0 (nothing to do here: a varlen
+// sequence with no row, or a prefill chunk of several rows, which the
+// per-row kernel takes), -1 (contract violation: NaN output).
+__device__ __forceinline__ int seq_decode_row(const int32_t* __restrict__ qsl, const int32_t* __restrict__ context_lens,
+                                              int max_context_len, int b, int& row, int& nv) {
+  nv = context_lens[b];
+  if (qsl == nullptr) {
+    row = b;
+    return (nv < 0 || nv > max_context_len) ? -1 : 1;
+  }
+  row = qsl[b];
+  if (qsl[b + 1] - row != 1) return 0;
+  return (nv < 1 || nv > max_context_len) ? -1 : 1;
+}
+
+// Log-sum-exp merge of the TPI lane rows of a wave for every head: on return
+// every lane holds, for head j, the wave's max M[j], sum L[j] and the
+// unnormalised output slice O[j][e] of its dims dl * VEC + e.
+template <typename T, int D, int S>
+__device__ __forceinline__ void merge_rows(const DecodeState<T, D, S>& st, float (&M)[S], float (&L)[S],
+                                           float (&O)[S][DecodeShape<T, D, S>::VEC]) {
+  using Sh = DecodeShape<T, D, S>;
+#pragma unroll
+  for (int j = 0; j < S; ++j) {
+    M[j] = across_groups_max<Sh::LPT>(st.m[j]);
+    const float w = fast_exp2(st.m[j] - M[j]);
+    L[j] = across_groups_sum<Sh::LPT>(st.l[j] * w);
+#pragma unroll
+    for (int e = 0; e < Sh::VEC; ++e) O[j][e] = across_groups_sum<Sh::LPT>(st.o[j][e] * w);
+  }
+}
+
+// Store the VEC consecutive outputs of one lane as one 16-byte vector store.
+__device__ __forceinline__ void store_vec(uint16_t* p, const float* v) {
+  u32x4 w;
+  w.x = (uint32_t)f32_to_bf16(v[0]) | (uint32_t)f32_to_bf16(v[1]) << 16;
+  w.y = (uint32_t)f32_to_bf16(v[2]) | (uint32_t)f32_to_bf16(v[3]) << 16;
+  w.z = (uint32_t)f32_to_bf16(v[4]) | (uint32_t)f32_to_bf16(v[5]) << 16;
+  w.w = (uint32_t)f32_to_bf16(v[6]) | (uint32_t)f32_to_bf16(v[7]) << 16;
+  *reinterpret_cast<u32x4*>(p) = w;
+}
+__device__ __forceinline__ void store_vec(float* p, const float* v) {
+  u32x4 w;
+  w.x = __float_as_uint(v[0]);
+  w.y = __float_as_uint(v[1]);
+  w.z = __float_as_uint(v[2]);
+  w.w = __float_as_uint(v[3]);
+  *reinterpret_cast<u32x4*>(p) = w;
+}
+
+// Finish one (row, KV head) item in place: out[j][d] = O[j][d] / L[j] for the
+// s heads, written by the lanes of row 0 (out points at head j = 0).
+template <typename T, int D, int S>
+__device__ __forceinline__ void finish_rows(const DecodeState<T, D, S>& st, int row, int dl, T* out) {
+  using Sh = DecodeShape<T, D, S>;
+  float M[S], L[S], O[S][Sh::VEC];
+  merge_rows<T, D, S>(st, M, L, O);
+  if (row == 0) {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      float v[Sh::VEC];
+#pragma unroll
+      for (int e = 0; e < Sh::VEC; ++e) v[e] = O[j][e] / L[j];
+      store_vec(out + j * D + dl * Sh::VEC, v);
+    }
+  }
+}
+
+// Partial record of one item: unnormalised O [S][D], then (M, L) per head.
+template <typename T, int D, int S>
+__device__ __forceinline__ void partial_rows(const DecodeState<T, D, S>& st, int row, int dl, int lane, float* o,
+                                             float* ml) {
+  using Sh = DecodeShape<T, D, S>;
+  float M[S], L[S], O[S][Sh::VEC];
+  merge_rows<T, D, S>(st, M, L, O);
+  if (row == 0) {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+#pragma unroll
+      for (int e = 0; e < Sh::VEC; e += 4) {
+        u32x4 w;
+        w.x = __float_as_uint(O[j][e]);
+        w.y = __float_as_uint(O[j][e + 1]);
+        w.z = __float_as_uint(O[j][e + 2]);
+        w.w = __float_as_uint(O[j][e + 3]);
+        *reinterpret_cast<u32x4*>(o + j * D + dl * Sh::VEC + e) = w;
+      }
+    }
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      ml[j * 2] = M[j];
+      ml[j * 2 + 1] = L[j];
+    }
+  }
+}
+
+}  // namespace pa

@@ -70,19 +70,37 @@ def dims(**kw):
     return pb.PaDims(**base)
 
 
+def _align(x):
+    return (x + 255) // 256 * 256
+
+
+def _stream_ws(B, H_q, D):
+    recs = 1024 * 2 * H_q  # (workgroup, slot) x (waves x group) = all query heads of a head block
+    return _align(recs * D * 4) + _align(recs * 2 * 4) + _align((B + 1) * 4)
+
+
+def _split_ws(rows, H_q, D, max_ctx, pps):
+    slots = -(-(-(-max_ctx // 16)) // pps)
+    if slots <= 1:
+        return 0
+    items = rows * H_q * slots
+    return _align(items * D * 4) + _align(items * 2 * 4)
+
+
 def test_workspace_size_formula():
-    # default granule 32 pages: 2048 tokens = 128 pages = 4 splits
-    n = pb.pa_workspace_size(dims())
-    items = 256 * 32 * 4
-    align = lambda x: (x + 255) // 256 * 256
-    assert n == align(items * 128 * 4) + align(items * 2 * 4)
-    # one split: no workspace
-    assert pb.pa_workspace_size(dims(max_context_len=512)) == 0
+    # library choice: the persistent stream-K path, partial records + prefix sums
+    assert pb.pa_workspace_size(dims()) == _stream_ws(256, 32, 128)
+    # explicit granule: the per-row split-K path (2048 tokens = 128 pages = 4 splits of 32)
+    assert pb.pa_workspace_size(dims(pages_per_split=32)) == _split_ws(256, 32, 128, 2048, 32)
+    assert pb.pa_workspace_size(dims(max_context_len=512, pages_per_split=32)) == 0
     assert pb.pa_workspace_size(dims(max_context_len=512, pages_per_split=8)) > 0
-    # varlen rows size the workspace
+    # varlen: stream records for the decode rows + split records for the prefill rows
     v = pb.pa_workspace_size(dims(num_q_rows=4608, max_q_len=512, num_seqs=520,
                                   max_context_len=4096, max_pages_per_seq=256))
-    assert v == align(4608 * 32 * 8 * 128 * 4) + align(4608 * 32 * 8 * 2 * 4)
+    assert v == _stream_ws(520, 32, 128) + _split_ws(4608, 32, 128, 4096, 128)
+    # too many sequences for the stream path's tables: split-K
+    big = dims(num_seqs=9000)
+    assert pb.pa_workspace_size(big) == _split_ws(9000, 32, 128, 2048, 128)
     assert pb.pa_workspace_size(dims(num_seqs=0)) >= 0
 
 

@@ -204,3 +204,31 @@ def test_full_size_mixed_sampled():
     sb, rows = sub_batch(b, seqs)
     ref = run_oracle(sb)
     assert_parity(got[rows], ref, strict=False, what="mixed")
+
+
+# --- stream-K vs split-K ----------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("s", [4, 6])
+def test_stream_and_split_paths_agree(dtype, s):
+    announce(f"stream vs split dtype={dtype} s={s}")
+    b = W.generate("dbrx-512", seed=21, dtype=dtype,
+                   overrides=dict(B=48, H_q=8 * s, ctx=("lognormal", 300, 1.2, 1, 3000)))
+    stream = run_gpu(b)                       # library choice: stream-K
+    split = run_gpu(b, pages_per_split=16)    # per-row split-K
+    scale = np.abs(split).max()
+    if dtype == "fp32":
+        assert np.abs(stream - split).max() <= 1e-5 * scale
+    sb, rows = sub_batch(b, list(range(0, 48, 3)))
+    ref = run_oracle(sb)
+    assert_parity(stream[rows], ref, what="stream")
+    assert_parity(split[rows], ref, what="split")
+
+
+def test_stream_handles_more_workgroups_than_pages():
+    # a few one-page sequences: most persistent workgroups get no units and
+    # items are cut into single units spread over many ranges
+    announce("stream tiny batch")
+    b = W.generate("tiny", seed=22, overrides=dict(H_q=32, H_kv=8, D=128,
+                                                   ctx=("list", [1, 5, 16, 17, 40, 3])))
+    assert_parity(run_gpu(b), run_oracle(b))
