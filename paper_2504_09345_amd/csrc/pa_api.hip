@@ -23,8 +23,10 @@ struct Plan {
   int W = 0, nb = 0;
   int64_t g_min = 0;  // persistent workgroups needed to keep every range within the LDS unit table
   size_t st_o = 0, st_ml = 0, st_cum = 0;
+  // MFMA prefill path (chunk rows of a varlen call)
+  bool prefill = false;
   // split-K path (all rows of a decode call that the stream path cannot take,
-  // or the chunked-prefill rows of a varlen call)
+  // or the chunked-prefill rows of a varlen call the MFMA path cannot take)
   bool split = false;
   int pps = 0;
   int n_split_slots = 0;
@@ -80,8 +82,10 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
     p->st_ml = align256(recs * 2 * sizeof(float));
     p->st_cum = align256(((size_t)d->num_seqs + 1) * sizeof(int32_t));
   }
-  // split-K for whatever the stream path does not take
-  p->split = varlen ? rows > 0 : !p->stream;
+  // chunked-prefill rows of a varlen call: MFMA kernel (bf16, head_dim 128)
+  p->prefill = varlen && p->stream && pa::prefill_supported(d->dtype, d->head_dim, s);
+  // split-K for whatever the stream and prefill paths do not take
+  p->split = varlen ? (rows > 0 && !p->prefill) : !p->stream;
   p->pps = d->pages_per_split > 0 ? d->pages_per_split : kDefaultPagesPerSplit;
   p->n_split_slots = (int)((max_pages + p->pps - 1) / p->pps);
   if (p->n_split_slots < 1) p->n_split_slots = 1;
@@ -94,7 +98,7 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
     }
   }
   if (rows == 0) {  // nothing to launch, nothing to hold
-    p->stream = p->split = false;
+    p->stream = p->split = p->prefill = false;
     p->st_o = p->st_ml = p->st_cum = p->sp_o = p->sp_ml = 0;
   }
   p->ws_bytes = p->st_o + p->st_ml + p->st_cum + p->sp_o + p->sp_ml;
@@ -167,6 +171,30 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
       e = pa::launch_stream(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream);
       if (e != hipSuccess) return PA_EHIP;
     }
+  }
+  if (p.prefill) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return PA_EHIP;
+    const int per_cu = pa::prefill_occupancy(p.s, dims->num_seqs);
+    if (per_cu <= 0) return PA_EHIP;
+    pa::PrefillArgs pf{};
+    pf.q = q;
+    pf.k_pages = k_pages;
+    pf.v_pages = v_pages;
+    pf.block_table = block_table;
+    pf.context_lens = context_lens;
+    pf.query_start_loc = query_start_loc;
+    pf.out = out;
+    pf.bt_stride = dims->max_pages_per_seq;
+    pf.scale_log2 = scale * 1.4426950408889634f;
+    pf.B = dims->num_seqs;
+    pf.H_q = dims->num_q_heads;
+    pf.H_kv = dims->num_kv_heads;
+    pf.max_context_len = dims->max_context_len;
+    e = pa::launch_prefill(p.s, pf, per_cu * cus, stream);
+    if (e != hipSuccess) return PA_EHIP;
   }
   pa::DecodeArgs a{};
   if (p.split) {

@@ -102,6 +102,24 @@ template <int G> __device__ __forceinline__ float across_groups_sum(float v) {
   }
 }
 
+// Exclusive prefix sum of one value per thread over a workgroup of NT
+// threads (Hillis-Steele in LDS; s_tmp holds NT ints).
+template <int NT>
+__device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp) {
+  const int tid = threadIdx.x;
+  s_tmp[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < NT; off <<= 1) {
+    const int add = tid >= off ? s_tmp[tid - off] : 0;
+    __syncthreads();
+    s_tmp[tid] += add;
+    __syncthreads();
+  }
+  const int incl = s_tmp[tid];
+  __syncthreads();
+  return incl - v;
+}
+
 // Block-table address function.  Token t of sequence b sits in slot t % 16 of
 // page block_table[b][t / 16]; the pool row of that token is page * 16 + slot
 // and, for KV head g of a [page][H_kv][16][D] pool, its first element is

@@ -81,6 +81,25 @@ hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, in
 hipError_t launch_stream_fixup(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
 int stream_occupancy(int dtype, int D, int s, int W);  // workgroups per CU, 0 on error
 
+// Arguments of the MFMA chunked-prefill kernel (bf16, head_dim 128): the rows
+// of every sequence with a chunk of L > 1 query rows.
+struct PrefillArgs {
+  const void* q;
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* block_table;
+  const int32_t* context_lens;
+  const int32_t* query_start_loc;
+  void* out;
+  int64_t bt_stride;
+  float scale_log2;
+  int B, H_q, H_kv, max_context_len;
+};
+
+bool prefill_supported(int dtype, int D, int s);
+int prefill_occupancy(int s, int B);  // workgroups per CU, 0 on error
+hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st);
+
 // dtype: 0 bf16, 1 fp32.  Return hipSuccess or the launch error.
 hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st);
 hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st);

@@ -37,22 +37,6 @@ __device__ __forceinline__ bool info_end(int i) { return (i >> 6) & 1; }
 __device__ __forceinline__ int info_hb(int i) { return (i >> 7) & 63; }
 __device__ __forceinline__ int info_row(int i) { return (int)((unsigned)i >> 13); }
 
-template <int NT>
-__device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp) {
-  const int tid = threadIdx.x;
-  s_tmp[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < NT; off <<= 1) {
-    const int add = tid >= off ? s_tmp[tid - off] : 0;
-    __syncthreads();
-    s_tmp[tid] += add;
-    __syncthreads();
-  }
-  const int incl = s_tmp[tid];
-  __syncthreads();
-  return incl - v;
-}
-
 template <typename T, int D, int S, int W, int NBUF>
 __global__ __launch_bounds__(64 * W) void stream_kernel(StreamArgs a) {
   using Sh = DecodeShape<T, D, S>;

@@ -94,10 +94,14 @@ def test_workspace_size_formula():
     assert pb.pa_workspace_size(dims(pages_per_split=32)) == _split_ws(256, 32, 128, 2048, 32)
     assert pb.pa_workspace_size(dims(max_context_len=512, pages_per_split=32)) == 0
     assert pb.pa_workspace_size(dims(max_context_len=512, pages_per_split=8)) > 0
-    # varlen: stream records for the decode rows + split records for the prefill rows
-    v = pb.pa_workspace_size(dims(num_q_rows=4608, max_q_len=512, num_seqs=520,
-                                  max_context_len=4096, max_pages_per_seq=256))
-    assert v == _stream_ws(520, 32, 128) + _split_ws(4608, 32, 128, 4096, 128)
+    # varlen bf16: stream records for the decode rows; the MFMA prefill kernel
+    # needs no workspace
+    vl = dict(num_q_rows=4608, max_q_len=512, num_seqs=520, max_context_len=4096,
+              max_pages_per_seq=256)
+    assert pb.pa_workspace_size(dims(**vl)) == _stream_ws(520, 32, 128)
+    # varlen fp32: chunk rows take the per-row split-K kernel
+    assert pb.pa_workspace_size(dims(dtype=pb.PA_FP32, **vl)) == (
+        _stream_ws(520, 32, 128) + _split_ws(4608, 32, 128, 4096, 128))
     # too many sequences for the stream path's tables: split-K
     big = dims(num_seqs=9000)
     assert pb.pa_workspace_size(big) == _split_ws(9000, 32, 128, 2048, 128)

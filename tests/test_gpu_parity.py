@@ -232,3 +232,49 @@ def test_stream_handles_more_workgroups_than_pages():
     b = W.generate("tiny", seed=22, overrides=dict(H_q=32, H_kv=8, D=128,
                                                    ctx=("list", [1, 5, 16, 17, 40, 3])))
     assert_parity(run_gpu(b), run_oracle(b))
+
+
+# --- MFMA chunked prefill ---------------------------------------------------
+
+def _chunk_batch(s, seed, chunks, decode_ctx, dtype="bf16", poison=False):
+    """Sequences with (chunk length L, prior cached tokens) plus decode rows,
+    interleaved, identity-free random page placement."""
+    rng = np.random.default_rng(seed)
+    seqs = [(L, prior) for L, prior in chunks] + [(1, c - 1) for c in decode_ctx]
+    order = rng.permutation(len(seqs))
+    seqs = [seqs[i] for i in order]
+    ctx = [L + prior for L, prior in seqs]
+    qlen = [L for L, _ in seqs]
+    b = W.generate("tiny", seed=seed, dtype=dtype, poison=poison,
+                   overrides=dict(H_q=2 * s, H_kv=2, D=128, ctx=("list", ctx), pool=("factor", 1.4)))
+    # re-draw q with one row per query position
+    T = int(sum(qlen))
+    q = W._fill_normal((T, 2 * s, 128), seed + 1, "q", 1.0, dtype, 1)
+    qsl = np.zeros(len(seqs) + 1, np.int32)
+    qsl[1:] = np.cumsum(qlen)
+    return W.Batch(**{**b.__dict__, "q": q, "query_start_loc": qsl})
+
+
+@pytest.mark.parametrize("s", [1, 2, 4, 6, 8])
+def test_prefill_chunks_mfma(s):
+    announce(f"prefill chunks s={s}")
+    chunks = [(2, 0), (17, 5), (32, 0), (33, 100), (100, 0), (64, 1000), (200, 37), (130, 700)]
+    b = _chunk_batch(s, 30 + s, chunks, decode_ctx=[1, 16, 300, 2000])
+    got = run_gpu(b)
+    ref = run_oracle(b)
+    assert_parity(got, ref, strict=False, what=f"prefill s={s}")
+
+
+def test_prefill_poisoned_pool():
+    announce("prefill poison")
+    b = _chunk_batch(4, 40, [(48, 7), (96, 300), (31, 0)], decode_ctx=[33, 500], poison=True)
+    got = run_gpu(b)
+    assert np.isfinite(got).all()
+    assert_parity(got, run_oracle(b), strict=False)
+
+
+def test_prefill_determinism_and_single_rows_match_decode():
+    announce("prefill determinism")
+    b = _chunk_batch(4, 41, [(64, 200), (7, 3)], decode_ctx=[100, 900])
+    a1, a2 = run_gpu(b), run_gpu(b)
+    assert np.array_equal(a1.view(np.uint32), a2.view(np.uint32))
