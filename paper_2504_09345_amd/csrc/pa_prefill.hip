@@ -169,8 +169,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
         if (pg * kPage + st_key < C) {
           const int32_t page = bt.page(b, pg);
           const int64_t off = ((int64_t)page * a.H_kv + g) * (int64_t)(kPage * D) + st_key * D + st_c8 * 4;
-          kr = *reinterpret_cast<const u32x2_t*>(kp + off);
-          vr = *reinterpret_cast<const u32x2_t*>(vp + off);
+          kr = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(kp + off));
+          vr = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(vp + off));
         } else {
           kr = u32x2_t{0, 0};
           vr = u32x2_t{0, 0};

@@ -65,15 +65,20 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const T* base, int v
                                            0x00020000);
 }
 
+// Cache policy of the K/V tile loads: non-temporal (each byte is read once
+// per call).  On MI355X this streams randomly placed 32 KiB pages at ~7.0
+// TB/s against ~6.2 TB/s with the default policy.
+constexpr int kKvLoadPolicy = 2;  // nt
+
 // Issue the NI K and NI V 16-byte-per-lane loads of one tile.  Lane l reads
 // bytes [16 l, 16 l + 16) of each 1 KiB slice: fully coalesced.
 template <int NI>
 __device__ __forceinline__ void issue_tile(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int lane_off,
                                            u32x4 (&k)[NI], u32x4 (&v)[NI]) {
 #pragma unroll
-  for (int i = 0; i < NI; ++i) k[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off, i * 1024, 0);
+  for (int i = 0; i < NI; ++i) k[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, lane_off, i * 1024, kKvLoadPolicy);
 #pragma unroll
-  for (int i = 0; i < NI; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, lane_off, i * 1024, 0);
+  for (int i = 0; i < NI; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, lane_off, i * 1024, kKvLoadPolicy);
 }
 
 // Fold one tile into the running state.  `valid` (wave-uniform) is the number
