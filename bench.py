@@ -22,6 +22,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import hashlib
 import json
 import os
 import sys
@@ -110,6 +111,22 @@ def to_device(a: np.ndarray, torch):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE passes, scaled by a known-size copy),
+    or None when there is none or the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", f"stream_kernel_{workload}_pmc.json")
+    if not os.path.exists(path):
+        return None, None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in rec["source_files"]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if h.hexdigest() != rec["source_sha256"]:
+        return None, os.path.relpath(path, ROOT) + " (stale: kernel changed)"
+    return int(rec["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
+
+
 def _cpu_baseline(batch: W.Batch, target_s: float, max_seqs: int | None):
     import oracle
     B = batch.num_seqs
@@ -135,12 +152,13 @@ def _cpu_baseline(batch: W.Batch, target_s: float, max_seqs: int | None):
     while dt < target_s / 3 and n < limit:
         n = min(limit, max(n + 1, int(n * min(8.0, (target_s / 3) / max(dt, 1e-3)))))
         dt = run(n)
-    reps = max(1, min(3, int(target_s / max(dt, 1e-3))))
+    # repeat the sample until about target_s of wall time is spent
+    reps = max(1, min(200, int(target_s / max(dt, 1e-3))))
     times = [dt] + [run(n) for _ in range(reps - 1)]
     t = float(np.median(times))
     return dict(value=n / t, unit="seqs/s", cores=oracle.get_threads(), kind="oracle",
-                sample=f"first {n} of {B} sequences of the same batch, median of {len(times)} runs "
-                       f"of {t:.2f} s (fp32 oracle, OpenMP)")
+                sample=f"first {n} of {B} sequences of the same batch, {len(times)} runs, "
+                       f"median {t:.3f} s per run (fp32 oracle, OpenMP over rows x heads)")
 
 
 def main():
@@ -231,6 +249,7 @@ def main():
         ev.destroy(m.attn_begin), ev.destroy(m.attn_end), ev.destroy(m.reduce_end)
 
     by = algorithmic_bytes(batch)
+    traffic, traffic_src = measured_traffic(args.workload) if args.pages_per_split == 0 else (None, None)
     fl = algorithmic_flops(batch)
     attn_avg_s = float(np.mean(attn_ms)) / 1e3
     achieved = by["total"] / attn_avg_s / 1e9
@@ -263,7 +282,9 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_unit": "bytes/launch",
+            "traffic_source": traffic_src,
         },
         "kernels": {
             "attention_us_mean": round(float(np.mean(attn_ms)) * 1e3, 2),

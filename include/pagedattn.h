@@ -99,9 +99,10 @@ typedef struct pa_dims {
 } pa_dims_t;
 
 /* Optional timing hooks: when a pa_timing_t* is passed and an event is
- * non-NULL, it is recorded on the call's stream at that point.  attn_begin
- * before the attention kernel, attn_end right after it, reduce_end after the
- * split-K reduction (recorded even when no reduction was needed). */
+ * non-NULL, it is recorded on the call's stream at that point: attn_begin
+ * before the first attention kernel, attn_end right after the attention
+ * kernel(s), reduce_end after the kernel that merges split partial results
+ * (recorded even when none was needed). */
 typedef struct pa_timing {
   hipEvent_t attn_begin;
   hipEvent_t attn_end;
@@ -109,13 +110,19 @@ typedef struct pa_timing {
 } pa_timing_t;
 
 /* Bytes of device workspace a paged_attn / paged_attn_varlen call with these
- * dims needs (split-K partial outputs and softmax statistics, plus the varlen
- * work list).  Writes 0 when no workspace is needed.  Host only; no HIP call.
+ * dims needs: partial outputs and softmax statistics of items split across
+ * workgroups, and per-sequence page prefix sums.  Writes 0 when no workspace
+ * is needed.  A call whose dims carry chunked rows (max_q_len > 1 or
+ * num_q_rows != num_seqs) is sized as varlen.  Host only; no HIP call.
  * Errors: PA_EINVAL / PA_ENOTSUP as for paged_attn. */
 int pa_workspace_size(const pa_dims_t *dims, size_t *bytes);
 
 /* Decode attention: one query row per sequence (Sec. 6.6 computes exactly
- * this on the CPU; here it is a split-K HIP kernel plus a reduction kernel).
+ * this on the CPU).  Here: a persistent stream-K kernel over equal ranges of
+ * (sequence, KV-head block, page) units plus a fixup kernel that merges the
+ * items cut by range boundaries; with pages_per_split > 0, or more than 8192
+ * sequences, a per-row split-K kernel plus a reduction kernel.  Both are
+ * deterministic (no float atomics).
  *   q            [num_seqs][H_q][D]        device, read
  *   k_pages,
  *   v_pages      pool, see layouts above   device, read
@@ -131,7 +138,9 @@ int paged_attn(const void *q, const void *k_pages, const void *v_pages,
                void *out, const pa_dims_t *dims, void *workspace, size_t workspace_bytes,
                hipStream_t stream, const pa_timing_t *timing);
 
-/* Mixed batch: causal prefill chunks and decode rows in one launch.
+/* Mixed batch: causal prefill chunks and decode rows in one call.  Decode
+ * rows take the stream-K kernel; chunk rows (L_b > 1) take an MFMA kernel
+ * (bf16, head_dim 128) or, otherwise, the per-row split-K kernel.
  * Same as paged_attn, with q/out of [num_q_rows][H_q][D] and the device array
  * query_start_loc (see layouts).  Row j of a chunk of length L in a sequence
  * of context C attends to positions 0 .. C - L + j.  dims->num_q_rows must
