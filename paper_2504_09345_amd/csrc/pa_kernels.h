@@ -76,6 +76,10 @@ constexpr int kStreamRing = PA_STREAM_RING;
 #define PA_STREAM_MAX_WAVES 8
 #endif
 constexpr int kStreamMaxWaves = PA_STREAM_MAX_WAVES;  // waves (KV heads) per stream workgroup
+#ifndef PA_STREAM_MFMA
+#define PA_STREAM_MFMA 1
+#endif
+constexpr bool kStreamMfma = PA_STREAM_MFMA != 0;  // bf16 D = 128 tiles on the matrix cores
 
 hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
 hipError_t launch_stream_fixup(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);

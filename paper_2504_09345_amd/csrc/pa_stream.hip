@@ -37,7 +37,7 @@ __device__ __forceinline__ bool info_end(int i) { return (i >> 6) & 1; }
 __device__ __forceinline__ int info_hb(int i) { return (i >> 7) & 63; }
 __device__ __forceinline__ int info_row(int i) { return (int)((unsigned)i >> 13); }
 
-template <typename T, int D, int S, int W, int NBUF>
+template <typename T, int D, int S, int W, int NBUF, bool MF>
 __global__ __launch_bounds__(64 * W) void stream_kernel(StreamArgs a) {
   using Sh = DecodeShape<T, D, S>;
   constexpr int NT = 64 * W;
@@ -107,6 +107,8 @@ __global__ __launch_bounds__(64 * W) void stream_kernel(StreamArgs a) {
   const T* qbase = reinterpret_cast<const T*>(a.q);
 
   DecodeState<T, D, S> st;
+  mfma::State<S> ms;  // matrix-core variant (bf16, D = 128)
+  __shared__ __attribute__((aligned(16))) uint8_t s_kv[MF ? W : 1][MF ? 2 * mfma::kTile : 16];
   bool head_partial = false;
 
   auto issue = [&](u32x4 (&kr)[Sh::NI], u32x4 (&vr)[Sh::NI], int k) {
@@ -134,29 +136,44 @@ __global__ __launch_bounds__(64 * W) void stream_kernel(StreamArgs a) {
         if (info_start(info) || k == 0) {  // a new (row, head) item: its queries
           head_partial = !info_start(info);
           const int g = info_hb(info) * W + w;
-          const T* qp = qbase + ((int64_t)info_row(info) * a.H_q + (int64_t)g * S) * D + dl * Sh::VEC;
+          const T* qg = qbase + ((int64_t)info_row(info) * a.H_q + (int64_t)g * S) * D;
+          if constexpr (MF) {
+            mfma::begin_item<S>(ms, reinterpret_cast<const uint16_t*>(qg), lane);
+          } else {
+            const T* qp = qg + dl * Sh::VEC;
 #pragma unroll
-          for (int j = 0; j < S; ++j) {
-            st.q[j] = *reinterpret_cast<const u32x4*>(qp + j * D);
-            st.m[j] = kMInit;
-            st.l[j] = 0.0f;
+            for (int j = 0; j < S; ++j) {
+              st.q[j] = *reinterpret_cast<const u32x4*>(qp + j * D);
+              st.m[j] = kMInit;
+              st.l[j] = 0.0f;
 #pragma unroll
-            for (int e = 0; e < Sh::VEC; ++e) st.o[j][e] = 0.0f;
+              for (int e = 0; e < Sh::VEC; ++e) st.o[j][e] = 0.0f;
+            }
           }
         }
       }
       issue(kr[(u + NBUF - 1) % NBUF], vr[(u + NBUF - 1) % NBUF], k + NBUF - 1);
       if (k < n_units) {
-        fold_tile<T, D, S>(st, kr[u], vr[u], row, info_valid(info), a.scale_log2);
+        if constexpr (MF)
+          mfma::fold<S>(ms, kr[u], vr[u], s_kv[w], lane, info_valid(info), a.scale_log2);
+        else
+          fold_tile<T, D, S>(st, kr[u], vr[u], row, info_valid(info), a.scale_log2);
         const bool tail_partial = k == n_units - 1 && !info_end(info);
         if (info_end(info) || k == n_units - 1) {
           const int r = info_row(info);
           const int g = info_hb(info) * W + w;
-          if (!head_partial && !tail_partial) {
-            finish_rows<T, D, S>(st, row, dl, reinterpret_cast<T*>(a.out) + ((int64_t)r * a.H_q + (int64_t)g * S) * D);
+          T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)r * a.H_q + (int64_t)g * S) * D;
+          const int64_t slot = ((int64_t)blockIdx.x * 2 + (head_partial ? 0 : 1)) * W + w;
+          if constexpr (MF) {
+            if (!head_partial && !tail_partial)
+              mfma::finish<S, T>(ms, lane, outp);
+            else
+              mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
           } else {
-            const int64_t slot = ((int64_t)blockIdx.x * 2 + (head_partial ? 0 : 1)) * W + w;
-            partial_rows<T, D, S>(st, row, dl, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
+            if (!head_partial && !tail_partial)
+              finish_rows<T, D, S>(st, row, dl, outp);
+            else
+              partial_rows<T, D, S>(st, row, dl, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
           }
         }
       }
@@ -230,7 +247,10 @@ __global__ __launch_bounds__(256) void stream_fixup_kernel(StreamArgs a, int G) 
 // ---- launchers -----------------------------------------------------------
 
 template <typename T, int D, int S, int W>
-static const void* stream_fn() { return reinterpret_cast<const void*>(&stream_kernel<T, D, S, W, kStreamRing>); }
+static const void* stream_fn() {
+  constexpr bool mf = kStreamMfma && sizeof(T) == 2 && D == 128;
+  return reinterpret_cast<const void*>(&stream_kernel<T, D, S, W, kStreamRing, mf>);
+}
 
 template <typename T, int D, int S>
 static const void* pick_w(int W) {

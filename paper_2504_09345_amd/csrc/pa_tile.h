@@ -262,4 +262,160 @@ __device__ __forceinline__ void partial_rows(const DecodeState<T, D, S>& st, int
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Matrix-core variant of the decode fold (bf16, head_dim 128).
+//
+// The s query heads of a group are the columns of a 16-wide MFMA tile (padded
+// with zero queries), the 16 tokens of a page its rows:
+//   S^T[token][head] = K . Q^T   4 x v_mfma_f32_16x16x32_bf16 (K as the A operand)
+//   O^T[dim][head]  += V^T . P^T 8 x 2 x v_mfma_f32_16x16x16_bf16 (P split into
+//                                bf16 high and low parts: fp32-level accuracy)
+// Lane l owns head column l % 16 and tokens 4 (l / 16) .. +3 of every tile, so
+// the softmax state and the rescale stay in the lane.  The wave stages each
+// tile through its own 8 KiB of LDS: K with 16-byte chunks XOR-swizzled by
+// token (conflict-free operand reads), V in natural order, read back as the
+// transposed PV operand with ds_read_b64_tr_b16 (lane j of a 16-lane group
+// receives element j % 4 of the 8-byte blocks addressed by lanes j / 4 + 4 i).
+namespace mfma {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+
+constexpr int kD = 128;
+constexpr int kTile = kPage * kD * 2;  // 4 KiB
+
+__device__ __forceinline__ int swz(int key, int chunk) { return key * (kD * 2) + ((chunk ^ (key & 15)) << 4); }
+
+template <int S>
+struct State {
+  u32x4 qt[kD / 32];   // Q^T operand: head lane%16 (zero when >= s), dims 32 st + 8 (lane/16) .. +8
+  f32x4_t acc[kD / 16];  // O^T: head lane%16, dims 16 mb + 4 (lane/16) + i
+  float m, l;          // running max (log2 units, shared by the 4 lanes of a head) and partial sum
+};
+
+template <int S>
+__device__ __forceinline__ void begin_item(State<S>& st, const uint16_t* q_group, int lane) {
+  const int n = lane & 15, G = lane >> 4;
+#pragma unroll
+  for (int s = 0; s < kD / 32; ++s)
+    st.qt[s] = n < S ? *reinterpret_cast<const u32x4*>(q_group + n * kD + s * 32 + G * 8) : u32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int mb = 0; mb < kD / 16; ++mb) st.acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  st.m = kMInit;
+  st.l = 0.0f;
+}
+
+__device__ __forceinline__ void split_hi_lo(const float (&p)[4], s16x4_t& hi, s16x4_t& lo) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t u = __float_as_uint(p[i]);
+    const uint32_t h = (u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u;
+    const uint32_t r = __float_as_uint(p[i] - __uint_as_float(h));
+    hi[i] = (short)(h >> 16);
+    lo[i] = (short)((r + 0x7fffu + ((r >> 16) & 1u)) >> 16);
+  }
+}
+
+// k / v: the tile as loaded (lane l: token l/16 + 4 i, 16-byte chunk l%16);
+// lds: this wave's 8 KiB (K then V); valid: live tokens of the tile.
+template <int S>
+__device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u32x4 (&v)[4], uint8_t* lds, int lane,
+                                     int valid, float scale_log2) {
+  const int G = lane >> 4, p = lane & 15;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = G + 4 * i;
+    *reinterpret_cast<u32x4*>(lds + swz(tok, p)) = k[i];
+    *reinterpret_cast<u32x4*>(lds + kTile + swz(tok, p)) = v[i];
+  }
+  // S^T = K . Q^T
+  f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int step = 0; step < kD / 32; ++step) {
+    const u32x4 ka = *reinterpret_cast<const u32x4*>(lds + swz(p, step * 4 + G));
+    s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka), __builtin_bit_cast(bf16x8_t, st.qt[step]),
+                                                s, 0, 0, 0);
+  }
+  // online softmax over this lane's 4 tokens, max shared by the head's 4 lanes
+  float x[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[i] = s[i] * scale_log2;
+    if (valid < kPage) x[i] = 4 * G + i < valid ? x[i] : -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  mx = fmaxf(mx, xor_lanes<16>(mx));
+  mx = fmaxf(mx, xor_lanes<32>(mx));
+  const float mnew = fmaxf(st.m, mx);
+  const float alpha = fast_exp2(st.m - mnew);
+  st.m = mnew;
+  float pw[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(x[i] - mnew);
+  st.l = fmaf(st.l, alpha, (pw[0] + pw[1]) + (pw[2] + pw[3]));
+  s16x4_t phi, plo;
+  split_hi_lo(pw, phi, plo);
+  // the O rescale is skipped when no head's max moved in this tile
+  const bool rescale = __builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0;
+  // O^T += V^T . P^T; lane p of group G addresses token 4 G + p / 4, dims 16 mb + 4 (p % 4)
+  const int vtok = 4 * G + (p >> 2);
+#pragma unroll
+  for (int mb = 0; mb < kD / 16; ++mb) {
+    const int d = mb * 16 + 4 * (p & 3);
+    const lds_s16x4_t* src = (const lds_s16x4_t*)(lds + kTile + swz(vtok, d >> 3) + (d & 7) * 2);
+    const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_s16x4_t*>(src));
+    if (rescale) st.acc[mb] *= alpha;
+    st.acc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, phi, st.acc[mb], 0, 0, 0);
+    st.acc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, plo, st.acc[mb], 0, 0, 0);
+  }
+}
+
+// Totals of the head column of this lane: L summed over the 4 lane groups.
+template <int S>
+__device__ __forceinline__ float total_l(const State<S>& st) {
+  float l = st.l;
+  l += xor_lanes<16>(l);
+  l += xor_lanes<32>(l);
+  return l;
+}
+
+// Finish an item in place: out points at head 0 of the group ([s][D]).
+template <int S, typename T>
+__device__ __forceinline__ void finish(const State<S>& st, int lane, T* out) {
+  const float L = total_l(st);
+  const int n = lane & 15, G = lane >> 4;
+  if (n < S) {
+    const float inv = 1.0f / L;
+#pragma unroll
+    for (int mb = 0; mb < kD / 16; ++mb) {
+      const int d = mb * 16 + 4 * G;
+      const uint32_t lo = (uint32_t)f32_to_bf16(st.acc[mb][0] * inv) | (uint32_t)f32_to_bf16(st.acc[mb][1] * inv) << 16;
+      const uint32_t hi = (uint32_t)f32_to_bf16(st.acc[mb][2] * inv) | (uint32_t)f32_to_bf16(st.acc[mb][3] * inv) << 16;
+      *reinterpret_cast<uint2*>(out + n * kD + d) = make_uint2(lo, hi);
+    }
+  }
+}
+
+// Partial record: unnormalised O [s][D] and (M, L) per head.
+template <int S>
+__device__ __forceinline__ void partial(const State<S>& st, int lane, float* o, float* ml) {
+  const float L = total_l(st);
+  const int n = lane & 15, G = lane >> 4;
+  if (n < S) {
+#pragma unroll
+    for (int mb = 0; mb < kD / 16; ++mb) {
+      const int d = mb * 16 + 4 * G;
+      *reinterpret_cast<f32x4_t*>(o + n * kD + d) = st.acc[mb];
+    }
+    if (G == 0) {
+      ml[n * 2] = st.m;
+      ml[n * 2 + 1] = L;
+    }
+  }
+}
+
+}  // namespace mfma
 }  // namespace pa

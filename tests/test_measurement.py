@@ -68,17 +68,26 @@ def test_bench_refuses_more_than_one_gpu():
     assert "one GPU" in json.loads(r.stdout)["error"]
 
 
-def test_traffic_is_dropped_when_kernel_changes(tmp_path, monkeypatch):
+def test_traffic_is_reported_only_for_the_measured_kernel(tmp_path, monkeypatch):
     rec = json.load(open(os.path.join(bench.ROOT, "profiles", "stream_kernel_mixtral-256_pmc.json")))
-    t, src = bench.measured_traffic("mixtral-256")
-    assert t == rec["traffic_bytes_per_launch"] and "stale" not in src
-    fake = tmp_path / "profiles"
-    fake.mkdir()
-    rec["source_sha256"] = "0" * 64
-    (fake / "stream_kernel_mixtral-256_pmc.json").write_text(json.dumps(rec))
     for f in rec["source_files"]:
         os.makedirs(tmp_path / os.path.dirname(f), exist_ok=True)
         (tmp_path / f).write_bytes(open(os.path.join(bench.ROOT, f), "rb").read())
+    (tmp_path / "profiles").mkdir()
+    import hashlib
+    h = hashlib.sha256()
+    for f in rec["source_files"]:
+        h.update((tmp_path / f).read_bytes())
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    # counters taken on exactly these sources: reported
+    rec["source_sha256"] = h.hexdigest()
+    (tmp_path / "profiles" / "stream_kernel_mixtral-256_pmc.json").write_text(json.dumps(rec))
+    t, src = bench.measured_traffic("mixtral-256")
+    assert t == rec["traffic_bytes_per_launch"] and "stale" not in src
+    # kernel changed since: dropped
+    rec["source_sha256"] = "0" * 64
+    (tmp_path / "profiles" / "stream_kernel_mixtral-256_pmc.json").write_text(json.dumps(rec))
     t2, src2 = bench.measured_traffic("mixtral-256")
     assert t2 is None and "stale" in src2
+    # no counters for a workload: nothing reported
+    assert bench.measured_traffic("tiny") == (None, None)
