@@ -127,7 +127,8 @@ int pa_workspace_size(const pa_dims_t *dims, size_t *bytes);
  *   k_pages,
  *   v_pages      pool, see layouts above   device, read
  *   block_table, context_lens              device, read
- *   scale        multiplies every dot product (typically 1/sqrt(D))
+ *   scale        multiplies every dot product (typically 1/sqrt(D)); must be
+ *                finite and > 0 (PA_EINVAL otherwise)
  *   out          [num_seqs][H_q][D]        device, written
  *   workspace    device scratch of at least pa_workspace_size() bytes (may
  *                be NULL when that size is 0); contents are overwritten

@@ -116,7 +116,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
   Plan p;
   int rc = plan(dims, varlen, &p);
   if (rc != PA_OK) return rc;
-  if (!isfinite(scale)) return PA_EINVAL;
+  if (!isfinite(scale) || !(scale > 0.0f)) return PA_EINVAL;
   if (p.rows > 0) {
     if (!q || !k_pages || !v_pages || !block_table || !context_lens || !out) return PA_EINVAL;
     if (varlen && !query_start_loc) return PA_EINVAL;

@@ -83,6 +83,36 @@ template <int OFF> __device__ __forceinline__ float xor_lanes(float v) {
   else return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (OFF << 10)));
 }
 
+// Lazy rebasing of the online softmax (matrix-core paths): a row's running
+// max m is moved only when a new score exceeds it by more than this many log2
+// units; until then weights exp2(x - m) stay below 2^kRescaleSlack and the
+// output accumulators need no rescale.  Any base gives the same normalised
+// result, since numerator and denominator share it.
+constexpr float kRescaleSlack = 8.0f;
+
+// Max / sum of v over the four 16-lane rows of the wave (lanes l, l ^ 16,
+// l ^ 32, l ^ 48), all lanes ending with the result.  gfx950's row-swap
+// permutes (v_permlane16_swap / v_permlane32_swap) run on the VALU: with the
+// same register as both operands, the swap returns rows (0, 0, 2, 2) and
+// (1, 1, 3, 3) (resp. halves (0, 0) and (1, 1)), so one max of the pair folds
+// the rows pairwise.
+__device__ __forceinline__ float rows4_max(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t um = __float_as_uint(m);
+  const auto b = __builtin_amdgcn_permlane32_swap(um, um, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float v) {
+  const uint32_t u = __float_as_uint(v);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float t = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t ut = __float_as_uint(t);
+  const auto b = __builtin_amdgcn_permlane32_swap(ut, ut, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // Max / sum across the aligned lane groups of size G that tile a wave: lane
 // l combines with l ^ G, l ^ 2G, ..., l ^ 32; every lane ends with the result.
 template <int G> __device__ __forceinline__ float across_groups_max(float v) {

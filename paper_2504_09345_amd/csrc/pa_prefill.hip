@@ -10,75 +10,58 @@
 //
 // Work item: (sequence, KV head g, block of PB chunk positions).  The block's
 // M = PB * s query rows (position-major, the s heads of group g) are split
-// over 8 waves of one 16-row MFMA block each.  Per 16-key page:
+// over 8 waves of two 16-row MFMA blocks each (256 rows), so every operand
+// read from LDS feeds two matrix products.  Per 16-key page:
 //   S^T[key][row] = K . Q^T   (v_mfma_f32_16x16x32_bf16, K as the A operand)
 //   online softmax per row (each lane owns one row and 4 of its keys)
-//   O^T[dim][row] += V^T . P^T (v_mfma_f32_16x16x16_bf16, P in bf16)
+//   O^T[dim][row] += V^T . P^T (v_mfma_f32_16x16x32_bf16 over 4 keys x the
+//                  bf16 high and low parts of P: fp32-level accuracy)
 // Computing the transposed products keeps "lane l % 16 = query row" in every
 // accumulator, so the softmax statistics, the P operand and the O rescale all
 // stay in the lane that owns the row: no register transposes.
 // The page's K and V tiles are staged in LDS once per workgroup and read by
-// all 8 waves: K with its 16-byte chunks XOR-swizzled by key (conflict-free
-// operand reads), V transposed to [dim][key] so that each lane's PV operand
-// (4 keys of one dim) is one 8-byte read.  Staging goes through registers,
-// two pages ahead, so the global loads overlap a full page of work.
+// all 8 waves, both with 16-byte chunks XOR-swizzled by key (conflict-free
+// operand reads); each lane's PV operand (4 keys of one dim) is one
+// ds_read_b64_tr_b16 from the naturally ordered V tile.  Staging goes through
+// two register sets, three pages ahead (a set is refilled right after it is
+// stored to LDS), and the item's block-table entries are read from an LDS
+// window, so global latency hides behind two pages of work.
 // A persistent grid walks the items in a snake order (item x and 2G-1-x per
 // workgroup) so early and late causal blocks pair up.
 #include "pa_device.h"
 #include "pa_kernels.h"
+#include "pa_tile.h"
 
 namespace pa {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
+using mfma::bf16x8_t;
+using mfma::f32x4_t;
+using mfma::lds_s16x4_t;
+using mfma::s16x4_t;
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 namespace {
 
 constexpr int kPfWaves = 8;
 constexpr int kPfThreads = 64 * kPfWaves;
-constexpr int kPfRows = 16 * kPfWaves;  // one 16-row MFMA block per wave
-
-// Byte offset, inside a swizzled [16 keys][D] bf16 tile, of the 16-byte chunk
-// c of key k: chunks of a key are permuted by XOR with the key.
-template <int D>
-__device__ __forceinline__ int swz_chunk(int k, int c) {
-  return k * (D * 2) + ((c ^ (k & 15)) << 4);
-}
-
-// Split four fp32 softmax weights into bf16 high parts (round to nearest
-// even) and bf16 low parts (the rounding residue, exact in fp32): hi + lo
-// carries ~16 mantissa bits, so the PV product keeps fp32-level accuracy
-// while both halves run on the bf16 matrix cores.
-__device__ __forceinline__ void split_bf16x4(const float (&p)[4], s16x4_t& hi, s16x4_t& lo) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t u = __float_as_uint(p[i]);
-    const uint32_t h = (u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u;
-    const uint32_t ur = __float_as_uint(p[i] - __uint_as_float(h));
-    hi[i] = (short)(h >> 16);
-    lo[i] = (short)((ur + 0x7fffu + ((ur >> 16) & 1u)) >> 16);
-  }
-}
+constexpr int kPfBlocks = 2;                       // 16-row MFMA blocks per wave
+constexpr int kPfRows = 16 * kPfBlocks * kPfWaves;  // 256 query rows per item
+constexpr int kPfMaxPages = 2048;                  // block-table window in LDS (power of 2)
 
 }  // namespace
 
 template <int D, int S>
 __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
-  static_assert(D == 128, "prefill MFMA path is built for head_dim 128");
+  static_assert(D == mfma::kD, "prefill MFMA path is built for head_dim 128");
   constexpr int PB = kPfRows / S;       // chunk positions per item
   constexpr int KSTEPS = D / 32;        // QK MFMA steps over dims
   constexpr int MB = D / 16;            // PV MFMA blocks over dims
-  constexpr int KT = kPage * D * 2;     // bytes of one K tile
-  constexpr int VT_STRIDE = kPage * 2 + 8;  // bytes per dim row of the V^T tile (padded)
-  constexpr int VT = D * VT_STRIDE;
-  constexpr int OUT_STRIDE = D * 2 + 16;
+  constexpr int KT = kPage * D * 2;     // bytes of one tile
   constexpr int C8 = D / 4;             // 8-byte chunks per key
 
   __shared__ __attribute__((aligned(16))) uint8_t s_k[2][KT];
-  __shared__ __attribute__((aligned(16))) uint8_t s_vt[2][VT];
-  __shared__ __attribute__((aligned(16))) uint8_t s_out[kPfRows * OUT_STRIDE];
+  __shared__ __attribute__((aligned(16))) uint8_t s_v[2][KT];
+  __shared__ int32_t s_bt[kPfMaxPages];
   __shared__ int32_t s_scan[kPfThreads];
   extern __shared__ int32_t s_cum[];  // [B + 1] prefix of items per sequence
 
@@ -112,7 +95,9 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
 
   // staging role of this thread: 8-byte chunk c8 of key st_key of a tile
   const int st_key = tid / C8, st_c8 = tid % C8;
-  const int m = w * 16 + (lane & 15);  // this lane's query row in the block
+  const int st_off = mfma::swz(st_key, st_c8 >> 1) + (st_c8 & 1) * 8;
+  const int st_ld = (st_key * D + st_c8 * 4) * 2;  // byte offset in the global tile
+  const int n = lane & 15, Gq = lane >> 4;  // MFMA column (query row of a block) and lane group
 
   for (int round = 0;; ++round) {
     const int x = (round & 1) ? G - 1 - blockIdx.x : blockIdx.x;
@@ -135,8 +120,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     const int npos = min(PB, L - pos0);           // valid positions in the block
     const bool bad = C > a.max_context_len || L > C || (C + kPage - 1) / kPage > (int)a.bt_stride;
 
+    __syncthreads();  // previous item's readers of s_k / s_v / s_bt are done
     if (bad) {  // contract violation: NaN rows, nothing read
-      __syncthreads();
       for (int idx = tid; idx < npos * S * D; idx += kPfThreads) {
         const int p = idx / (S * D), hd = idx % (S * D);
         og[((int64_t)(q0 + pos0 + p) * a.H_q + (int64_t)g * S) * D + hd] = 0x7fc0;
@@ -145,130 +130,164 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     }
     const int lim0 = C - L + pos0;                // last key of the block's first row
     const int npg = (lim0 + npos - 1) / kPage + 1;
+    // block-table window: s_bt[p % kPfMaxPages] holds the entry of page p
+    for (int i = tid; i < min(npg, kPfMaxPages); i += kPfThreads) s_bt[i] = bt.page(b, i);
 
-    const int p = m / S, h = m - p * S;
-    const bool valid = p < npos;
-    const int lim = valid ? lim0 + p : -1;
-    float mrow = kMInit, lrow = 0.0f;
-    f32x4_t acc[MB];
+    // this lane's rows: block rb, row m = (w * 2 + rb) * 16 + lane % 16
+    u32x4 qt[kPfBlocks][KSTEPS];
+    int lim[kPfBlocks];
+    float mrow[kPfBlocks], lrow[kPfBlocks];
+    f32x4_t acc[kPfBlocks][MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    u32x4 qt[KSTEPS];
-    {
+    for (int rb = 0; rb < kPfBlocks; ++rb) {
+      const int m = (w * kPfBlocks + rb) * 16 + n;
+      const int p = m / S, h = m - p * S;
+      const bool valid = p < npos;
+      lim[rb] = valid ? lim0 + p : -1;
+      mrow[rb] = kMInit;
+      lrow[rb] = 0.0f;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) acc[rb][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       const uint16_t* qrow = qg + ((int64_t)(q0 + pos0 + (valid ? p : 0)) * a.H_q + (int64_t)g * S + h) * D;
 #pragma unroll
       for (int st = 0; st < KSTEPS; ++st)
-        qt[st] = valid ? *reinterpret_cast<const u32x4*>(qrow + st * 32 + (lane >> 4) * 8) : u32x4{0, 0, 0, 0};
+        qt[rb][st] = valid ? *reinterpret_cast<const u32x4*>(qrow + st * 32 + Gq * 8) : u32x4{0, 0, 0, 0};
     }
+    __syncthreads();  // s_bt is filled
 
     // Slots past the context (the tail of the last page) are staged as zeros:
     // their weights are 0, but the matrix product would still form 0 * V for
     // them, and those bytes may hold anything.
+    // Loads, stores and the block-table read run unconditionally (no branch
+    // the compiler's wait counting has to merge): a page at or past npg is a
+    // null tile, staged as zeros and fully masked.
     auto fetch = [&](int pg, u32x2_t& kr, u32x2_t& vr) {
-      if (pg < npg) {
-        if (pg * kPage + st_key < C) {
-          const int32_t page = bt.page(b, pg);
-          const int64_t off = ((int64_t)page * a.H_kv + g) * (int64_t)(kPage * D) + st_key * D + st_c8 * 4;
-          kr = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(kp + off));
-          vr = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(vp + off));
-        } else {
-          kr = u32x2_t{0, 0};
-          vr = u32x2_t{0, 0};
-        }
-      }
+      // buffer loads past `valid` keys (all of them for pg >= npg) return 0
+      const int valid = pg < npg ? min(kPage, C - pg * kPage) : 0;
+      const int32_t entry = __builtin_amdgcn_readfirstlane(s_bt[pg & (kPfMaxPages - 1)]);
+      const int32_t page = pg < npg ? entry : 0;
+      const int64_t tile = ((int64_t)page * a.H_kv + g) * (int64_t)(kPage * D);
+      const __amdgpu_buffer_rsrc_t rk = tile_rsrc<uint16_t, D>(kp + tile, valid);
+      const __amdgpu_buffer_rsrc_t rv = tile_rsrc<uint16_t, D>(vp + tile, valid);
+      kr = __builtin_amdgcn_raw_buffer_load_b64(rk, st_ld, 0, kKvLoadPolicy);
+      vr = __builtin_amdgcn_raw_buffer_load_b64(rv, st_ld, 0, kKvLoadPolicy);
     };
     auto stash = [&](int pg, const u32x2_t& kr, const u32x2_t& vr) {
-      if (pg < npg) {
-        uint8_t* kt = s_k[pg & 1];
-        *reinterpret_cast<u32x2_t*>(kt + swz_chunk<D>(st_key, st_c8 >> 1) + (st_c8 & 1) * 8) = kr;
-        uint8_t* vt = s_vt[pg & 1] + st_key * 2;
-        const int d0 = st_c8 * 4;
-        *reinterpret_cast<uint16_t*>(vt + (d0 + 0) * VT_STRIDE) = (uint16_t)(vr.x & 0xffff);
-        *reinterpret_cast<uint16_t*>(vt + (d0 + 1) * VT_STRIDE) = (uint16_t)(vr.x >> 16);
-        *reinterpret_cast<uint16_t*>(vt + (d0 + 2) * VT_STRIDE) = (uint16_t)(vr.y & 0xffff);
-        *reinterpret_cast<uint16_t*>(vt + (d0 + 3) * VT_STRIDE) = (uint16_t)(vr.y >> 16);
-      }
+      *reinterpret_cast<u32x2_t*>(s_k[pg & 1] + st_off) = kr;
+      *reinterpret_cast<u32x2_t*>(s_v[pg & 1] + st_off) = vr;
     };
     auto consume = [&](int pg) {
       const uint8_t* kt = s_k[pg & 1];
-      const uint8_t* vt = s_vt[pg & 1];
-      // S^T = K . Q^T (A: key lane%16, dims 32 st + 8 (lane/16) .. +8)
-      f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      const uint8_t* vt = s_v[pg & 1];
+      // S^T = K . Q^T (A: key lane%16, dims 32 st + 8 (lane/16) .. +8), shared by both blocks
+      f32x4_t sc[kPfBlocks];
+#pragma unroll
+      for (int rb = 0; rb < kPfBlocks; ++rb) sc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < KSTEPS; ++st) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + swz_chunk<D>(lane & 15, st * 4 + (lane >> 4)));
-        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kv),
-                                                    __builtin_bit_cast(bf16x8_t, qt[st]), s, 0, 0, 0);
-      }
-      // online softmax: this lane holds keys 4 (lane/16) + i of row m
-      float xs[4];
-      const bool need_mask = pg * kPage + kPage - 1 > lim0;
+        const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + mfma::swz(n, st * 4 + Gq));
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        xs[i] = s[i] * a.scale_log2;
-        if (need_mask) xs[i] = pg * kPage + (lane >> 4) * 4 + i <= lim ? xs[i] : -INFINITY;
+        for (int rb = 0; rb < kPfBlocks; ++rb)
+          sc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kv),
+                                                           __builtin_bit_cast(bf16x8_t, qt[rb][st]), sc[rb], 0, 0, 0);
       }
-      float mx = fmaxf(fmaxf(xs[0], xs[1]), fmaxf(xs[2], xs[3]));
-      mx = fmaxf(mx, xor_lanes<16>(mx));
-      mx = fmaxf(mx, xor_lanes<32>(mx));
-      const float mnew = fmaxf(mrow, mx);
-      const float alpha = fast_exp2(mrow - mnew);
-      mrow = mnew;
-      float pw[4];
+      // online softmax per block: this lane holds keys 4 (lane/16) + i of its
+      // row; the causal mask applies on the pages that cross the diagonal
+      const bool diag = pg * kPage + kPage - 1 > lim0;
+      float xs[kPfBlocks][4], mc[kPfBlocks];
+      bool grow = false;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(xs[i] - mnew);
-      lrow = fmaf(lrow, alpha, (pw[0] + pw[1]) + (pw[2] + pw[3]));
-      s16x4_t phi, plo;
-      split_bf16x4(pw, phi, plo);
-      // O^T += V^T . P^T (A: dim 16 mb + lane%16, keys 4 (lane/16) .. +4)
+      for (int rb = 0; rb < kPfBlocks; ++rb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          xs[rb][i] = sc[rb][i];
+          if (diag) xs[rb][i] = pg * kPage + Gq * 4 + i <= lim[rb] ? xs[rb][i] : -INFINITY;
+        }
+        // scale > 0, so the max commutes with it
+        const float mx = rows4_max(fmaxf(fmaxf(xs[rb][0], xs[rb][1]), fmaxf(xs[rb][2], xs[rb][3]))) * a.scale_log2;
+        mc[rb] = fmaxf(mrow[rb], mx);
+        grow |= mc[rb] > mrow[rb] + kRescaleSlack;
+      }
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // rebase every row of the wave
+#pragma unroll
+        for (int rb = 0; rb < kPfBlocks; ++rb) {
+          const float alpha = fast_exp2(mrow[rb] - mc[rb]);
+          mrow[rb] = mc[rb];
+          lrow[rb] *= alpha;
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) acc[rb][mb] *= alpha;
+        }
+      }
+      s16x4_t phi[kPfBlocks], plo[kPfBlocks];
+#pragma unroll
+      for (int rb = 0; rb < kPfBlocks; ++rb) {
+        float pw[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(xs[rb][i], a.scale_log2, -mrow[rb]));
+        lrow[rb] += (pw[0] + pw[1]) + (pw[2] + pw[3]);
+        mfma::split_hi_lo(pw, phi[rb], plo[rb]);
+      }
+      // O^T += V^T . P^T; lane p of group Gq addresses key 4 Gq + p / 4, dims 16 mb + 4 (p % 4)
+      const int vkey = 4 * Gq + (n >> 2);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
-        const u32x2_t vv = *reinterpret_cast<const u32x2_t*>(vt + (mb * 16 + (lane & 15)) * VT_STRIDE + (lane >> 4) * 8);
-        const s16x4_t va = __builtin_bit_cast(s16x4_t, vv);
-        acc[mb] *= alpha;
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, phi, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, plo, acc[mb], 0, 0, 0);
+        const int d = mb * 16 + 4 * (n & 3);
+        const lds_s16x4_t* src = (const lds_s16x4_t*)(vt + mfma::swz(vkey, d >> 3) + (d & 7) * 2);
+        const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_s16x4_t*>(src));
+#pragma unroll
+        for (int rb = 0; rb < kPfBlocks; ++rb) acc[rb][mb] = mfma::pv_mfma(va, phi[rb], plo[rb], acc[rb][mb]);
       }
     };
 
-    u32x2_t kr0 = {0, 0}, vr0 = {0, 0}, kr1 = {0, 0}, vr1 = {0, 0};
-    __syncthreads();  // previous item's readers of s_k / s_vt / s_out are done
-    fetch(0, kr0, vr0);
-    fetch(1, kr1, vr1);
-    stash(0, kr0, vr0);
-    for (int pg = 0; pg < npg; pg += 2) {
-      __syncthreads();  // page pg is in LDS; everyone is done with page pg-1
-      stash(pg + 1, kr1, vr1);
-      fetch(pg + 2, kr0, vr0);
-      consume(pg);
-      if (pg + 1 < npg) {
+    // Page p is staged through register set p & 1: page pg + 1 is stored to
+    // LDS while page pg is consumed, and its set is at once refilled with page
+    // pg + 3, so pages pg + 2 and pg + 3 are in flight meanwhile.
+    auto page_barrier = [&](int pg) {
+      __syncthreads();  // page pg is in LDS; everyone is done with page pg - 1
+      if (((pg + 3) & (kPfMaxPages - 1)) == 0 && pg + 3 < npg) {
+        // slide the block-table window to pages pg + 3 .. pg + 3 + kPfMaxPages - 1
+        for (int i = tid; i < min(npg - (pg + 3), kPfMaxPages); i += kPfThreads) s_bt[i] = bt.page(b, pg + 3 + i);
         __syncthreads();
-        stash(pg + 2, kr0, vr0);
-        fetch(pg + 3, kr1, vr1);
-        consume(pg + 1);
       }
+    };
+    u32x2_t ka, va, kb, vb;
+    // (scheduling barriers keep the issue order the loop's waits assume)
+    fetch(0, ka, va);
+    fetch(1, kb, vb);
+    __builtin_amdgcn_sched_barrier(0);
+    stash(0, ka, va);
+    __builtin_amdgcn_sched_barrier(0);
+    fetch(2, ka, va);
+    __builtin_amdgcn_sched_barrier(0);
+    // two pages per trip; with npg odd the last trip's second page is null
+    for (int pg = 0; pg < npg; pg += 2) {
+      page_barrier(pg);
+      stash(pg + 1, kb, vb);
+      fetch(pg + 3, kb, vb);
+      consume(pg);
+      page_barrier(pg + 1);
+      stash(pg + 2, ka, va);
+      fetch(pg + 4, ka, va);
+      consume(pg + 1);
     }
 
-    // normalise and stage the block's rows in LDS (row m: position m/S, head m%S)
-    float l = lrow;
-    l += xor_lanes<16>(l);
-    l += xor_lanes<32>(l);
-    const float inv = valid ? 1.0f / l : 0.0f;
+    // normalise and store straight from the accumulators: lane (n, Gq) holds
+    // dims 16 mb + 4 Gq + i of row (w * 2 + rb) * 16 + n
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+    for (int rb = 0; rb < kPfBlocks; ++rb) {
+      const float l = rows4_sum(lrow[rb]);
+      if (lim[rb] >= 0) {
+        const float inv = 1.0f / l;
+        const int m = (w * kPfBlocks + rb) * 16 + n;
+        const int p = m / S, h = m - p * S;
+        uint16_t* orow = og + ((int64_t)(q0 + pos0 + p) * a.H_q + (int64_t)g * S + h) * D;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = mb * 16 + (lane >> 4) * 4 + i;
-        *reinterpret_cast<uint16_t*>(s_out + m * OUT_STRIDE + d * 2) = f32_to_bf16(acc[mb][i] * inv);
+        for (int mb = 0; mb < MB; ++mb) {
+          const uint32_t w0 = (uint32_t)f32_to_bf16(acc[rb][mb][0] * inv) | (uint32_t)f32_to_bf16(acc[rb][mb][1] * inv) << 16;
+          const uint32_t w1 = (uint32_t)f32_to_bf16(acc[rb][mb][2] * inv) | (uint32_t)f32_to_bf16(acc[rb][mb][3] * inv) << 16;
+          *reinterpret_cast<u32x2_t*>(orow + mb * 16 + 4 * Gq) = u32x2_t{w0, w1};
+        }
       }
-    __syncthreads();
-    // coalesced stores: 16 bytes per thread per step
-    constexpr int CHUNKS = D / 8;
-    for (int idx = tid; idx < npos * S * CHUNKS; idx += kPfThreads) {
-      const int mm = idx / CHUNKS, c = idx % CHUNKS;
-      const int pp = mm / S, hh = mm - pp * S;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(s_out + mm * OUT_STRIDE + c * 16);
-      *reinterpret_cast<u32x4*>(og + ((int64_t)(q0 + pos0 + pp) * a.H_q + (int64_t)g * S + hh) * D + c * 8) = v;
     }
   }
 }

@@ -269,8 +269,9 @@ __device__ __forceinline__ void partial_rows(const DecodeState<T, D, S>& st, int
 // The s query heads of a group are the columns of a 16-wide MFMA tile (padded
 // with zero queries), the 16 tokens of a page its rows:
 //   S^T[token][head] = K . Q^T   4 x v_mfma_f32_16x16x32_bf16 (K as the A operand)
-//   O^T[dim][head]  += V^T . P^T 8 x 2 x v_mfma_f32_16x16x16_bf16 (P split into
-//                                bf16 high and low parts: fp32-level accuracy)
+//   O^T[dim][head]  += V^T . P^T 8 x v_mfma_f32_16x16x32_bf16 (P split into bf16
+//                                high and low parts for fp32-level accuracy;
+//                                the k dimension holds 4 tokens x {hi, lo})
 // Lane l owns head column l % 16 and tokens 4 (l / 16) .. +3 of every tile, so
 // the softmax state and the rescale stay in the lane.  The wave stages each
 // tile through its own 8 KiB of LDS: K with 16-byte chunks XOR-swizzled by
@@ -282,6 +283,7 @@ namespace mfma {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int kD = 128;
@@ -293,7 +295,7 @@ template <int S>
 struct State {
   u32x4 qt[kD / 32];   // Q^T operand: head lane%16 (zero when >= s), dims 32 st + 8 (lane/16) .. +8
   f32x4_t acc[kD / 16];  // O^T: head lane%16, dims 16 mb + 4 (lane/16) + i
-  float m, l;          // running max (log2 units, shared by the 4 lanes of a head) and partial sum
+  float m, l;          // softmax base (log2 units, shared by the 4 lanes of a head) and partial sum
 };
 
 template <int S>
@@ -308,15 +310,33 @@ __device__ __forceinline__ void begin_item(State<S>& st, const uint16_t* q_group
   st.l = 0.0f;
 }
 
+// Split four fp32 softmax weights into bf16 high parts (round to nearest
+// even) and bf16 low parts (the rounding residue, exact in fp32): hi + lo
+// carries ~16 mantissa bits, so the PV product keeps fp32-level accuracy
+// while both halves run on the bf16 matrix cores.  Conversions are gfx950's
+// v_cvt_pk_bf16_f32 (two values per instruction, nearest even).
 __device__ __forceinline__ void split_hi_lo(const float (&p)[4], s16x4_t& hi, s16x4_t& lo) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t u = __float_as_uint(p[i]);
-    const uint32_t h = (u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u;
-    const uint32_t r = __float_as_uint(p[i] - __uint_as_float(h));
-    hi[i] = (short)(h >> 16);
-    lo[i] = (short)((r + 0x7fffu + ((r >> 16) & 1u)) >> 16);
-  }
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+  const f32x2_t p01 = f32x2_t{p[0], p[1]}, p23 = f32x2_t{p[2], p[3]};
+  const bf16x2v_t h01 = __builtin_convertvector(p01, bf16x2v_t);
+  const bf16x2v_t h23 = __builtin_convertvector(p23, bf16x2v_t);
+  const bf16x2v_t l01 = __builtin_convertvector(p01 - __builtin_convertvector(h01, f32x2_t), bf16x2v_t);
+  const bf16x2v_t l23 = __builtin_convertvector(p23 - __builtin_convertvector(h23, f32x2_t), bf16x2v_t);
+  // whole-vector bit casts only (a bit cast of one vector element misreads)
+  hi = __builtin_bit_cast(s16x4_t, u32x2_t{__builtin_bit_cast(uint32_t, h01), __builtin_bit_cast(uint32_t, h23)});
+  lo = __builtin_bit_cast(s16x4_t, u32x2_t{__builtin_bit_cast(uint32_t, l01), __builtin_bit_cast(uint32_t, l23)});
+}
+
+// acc += V^T . (P_hi + P_lo)^T in one 16x16x32 product: the lane's k slots
+// 8 G .. 8 G + 7 carry its 4 tokens twice in A (va = V^T of tokens 4 G + i)
+// and P's high then low parts in B, so the sum over k adds both products.
+__device__ __forceinline__ f32x4_t pv_mfma(const s16x4_t& va, const s16x4_t& phi, const s16x4_t& plo, f32x4_t acc) {
+  const s16x8_t a = __builtin_shufflevector(va, va, 0, 1, 2, 3, 0, 1, 2, 3);
+  const s16x8_t b = __builtin_shufflevector(phi, plo, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), acc,
+                                                 0, 0, 0);
 }
 
 // k / v: the tile as loaded (lane l: token l/16 + 4 i, 16-byte chunk l%16);
@@ -339,27 +359,30 @@ __device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u3
     s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka), __builtin_bit_cast(bf16x8_t, st.qt[step]),
                                                 s, 0, 0, 0);
   }
-  // online softmax over this lane's 4 tokens, max shared by the head's 4 lanes
+  // online softmax over this lane's 4 tokens, max shared by the head's 4
+  // lanes; the base moves only past the slack (the branch is wave-uniform)
   float x[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    x[i] = s[i] * scale_log2;
+    x[i] = s[i];
     if (valid < kPage) x[i] = 4 * G + i < valid ? x[i] : -INFINITY;
   }
-  float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-  mx = fmaxf(mx, xor_lanes<16>(mx));
-  mx = fmaxf(mx, xor_lanes<32>(mx));
-  const float mnew = fmaxf(st.m, mx);
-  const float alpha = fast_exp2(st.m - mnew);
-  st.m = mnew;
+  // scale > 0, so the max commutes with it
+  const float mx = rows4_max(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]))) * scale_log2;
+  const float mc = fmaxf(st.m, mx);
+  if (__builtin_amdgcn_ballot_w64(mc > st.m + kRescaleSlack) != 0) {
+    const float alpha = fast_exp2(st.m - mc);
+    st.m = mc;
+    st.l *= alpha;
+#pragma unroll
+    for (int mb = 0; mb < kD / 16; ++mb) st.acc[mb] *= alpha;
+  }
   float pw[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(x[i] - mnew);
-  st.l = fmaf(st.l, alpha, (pw[0] + pw[1]) + (pw[2] + pw[3]));
+  for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(x[i], scale_log2, -st.m));
+  st.l += (pw[0] + pw[1]) + (pw[2] + pw[3]);
   s16x4_t phi, plo;
   split_hi_lo(pw, phi, plo);
-  // the O rescale is skipped when no head's max moved in this tile
-  const bool rescale = __builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0;
   // O^T += V^T . P^T; lane p of group G addresses token 4 G + p / 4, dims 16 mb + 4 (p % 4)
   const int vtok = 4 * G + (p >> 2);
 #pragma unroll
@@ -367,19 +390,14 @@ __device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u3
     const int d = mb * 16 + 4 * (p & 3);
     const lds_s16x4_t* src = (const lds_s16x4_t*)(lds + kTile + swz(vtok, d >> 3) + (d & 7) * 2);
     const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_s16x4_t*>(src));
-    if (rescale) st.acc[mb] *= alpha;
-    st.acc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, phi, st.acc[mb], 0, 0, 0);
-    st.acc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(va, plo, st.acc[mb], 0, 0, 0);
+    st.acc[mb] = pv_mfma(va, phi, plo, st.acc[mb]);
   }
 }
 
 // Totals of the head column of this lane: L summed over the 4 lane groups.
 template <int S>
 __device__ __forceinline__ float total_l(const State<S>& st) {
-  float l = st.l;
-  l += xor_lanes<16>(l);
-  l += xor_lanes<32>(l);
-  return l;
+  return rows4_sum(st.l);
 }
 
 // Finish an item in place: out points at head 0 of the group ([s][D]).

@@ -132,7 +132,8 @@ FAKE = 0x1000  # never dereferenced: every call below fails validation first
 
 @host_only
 @pytest.mark.parametrize("case", ["null_q", "null_out", "bad_group", "small_ws", "no_ws",
-                                  "nan_scale", "decode_rows", "decode_qlen", "hd"])
+                                  "nan_scale", "zero_scale", "neg_scale", "decode_rows",
+                                  "decode_qlen", "hd"])
 def test_paged_attn_validation(case):
     d = dims()
     args = dict(q=FAKE, k=FAKE, v=FAKE, bt=FAKE, cl=FAKE, scale=0.088, out=FAKE, ws=FAKE,
@@ -152,6 +153,10 @@ def test_paged_attn_validation(case):
         expect = pb.PA_ENOSPC
     elif case == "nan_scale":
         args["scale"] = float("nan")
+    elif case == "zero_scale":
+        args["scale"] = 0.0
+    elif case == "neg_scale":
+        args["scale"] = -0.088
     elif case == "decode_rows":
         d.num_q_rows = 7
     elif case == "decode_qlen":
