@@ -47,6 +47,7 @@ constexpr int kPfThreads = 64 * kPfWaves;
 constexpr int kPfBlocks = 2;                       // 16-row MFMA blocks per wave
 constexpr int kPfRows = 16 * kPfBlocks * kPfWaves;  // 256 query rows per item
 constexpr int kPfMaxPages = 2048;                  // block-table window in LDS (power of 2)
+constexpr int kPfStep = 2;                         // pages per synchronised step
 
 }  // namespace
 
@@ -57,10 +58,11 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   constexpr int KSTEPS = D / 32;        // QK MFMA steps over dims
   constexpr int MB = D / 16;            // PV MFMA blocks over dims
   constexpr int KT = kPage * D * 2;     // bytes of one tile
-  constexpr int C8 = D / 4;             // 8-byte chunks per key
+  constexpr int C16 = D / 8;            // 16-byte chunks per key
+  static_assert(kPfStep * kPage * C16 == kPfThreads, "one 16-byte chunk of K and V per thread and step");
 
-  __shared__ __attribute__((aligned(16))) uint8_t s_k[2][KT];
-  __shared__ __attribute__((aligned(16))) uint8_t s_v[2][KT];
+  __shared__ __attribute__((aligned(16))) uint8_t s_k[2][kPfStep * KT];
+  __shared__ __attribute__((aligned(16))) uint8_t s_v[2][kPfStep * KT];
   __shared__ int32_t s_bt[kPfMaxPages];
   __shared__ int32_t s_scan[kPfThreads];
   extern __shared__ int32_t s_cum[];  // [B + 1] prefix of items per sequence
@@ -93,10 +95,12 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const uint16_t* qg = reinterpret_cast<const uint16_t*>(a.q);
   uint16_t* og = reinterpret_cast<uint16_t*>(a.out);
 
-  // staging role of this thread: 8-byte chunk c8 of key st_key of a tile
-  const int st_key = tid / C8, st_c8 = tid % C8;
-  const int st_off = mfma::swz(st_key, st_c8 >> 1) + (st_c8 & 1) * 8;
-  const int st_ld = (st_key * D + st_c8 * 4) * 2;  // byte offset in the global tile
+  // staging role of this thread: 16-byte chunk st_c of key st_key of page
+  // st_pg of a step (st_pg is wave-uniform)
+  const int st_pg = w / (kPfWaves / kPfStep), st_j = tid % (kPage * C16);
+  const int st_key = st_j / C16, st_c = st_j % C16;
+  const int st_off = st_pg * KT + mfma::swz(st_key, st_c);
+  const int st_ld = st_j * 16;  // byte offset in the global tile
   const int n = lane & 15, Gq = lane >> 4;  // MFMA column (query row of a block) and lane group
 
   for (int round = 0;; ++round) {
@@ -161,7 +165,9 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     // Loads, stores and the block-table read run unconditionally (no branch
     // the compiler's wait counting has to merge): a page at or past npg is a
     // null tile, staged as zeros and fully masked.
-    auto fetch = [&](int pg, u32x2_t& kr, u32x2_t& vr) {
+    const int nst = (npg + kPfStep - 1) / kPfStep;  // steps of kPfStep pages
+    auto fetch = [&](int t, u32x4& kr, u32x4& vr) {
+      const int pg = t * kPfStep + st_pg;
       // buffer loads past `valid` keys (all of them for pg >= npg) return 0
       const int valid = pg < npg ? min(kPage, C - pg * kPage) : 0;
       const int32_t entry = __builtin_amdgcn_readfirstlane(s_bt[pg & (kPfMaxPages - 1)]);
@@ -169,43 +175,52 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       const int64_t tile = ((int64_t)page * a.H_kv + g) * (int64_t)(kPage * D);
       const __amdgpu_buffer_rsrc_t rk = tile_rsrc<uint16_t, D>(kp + tile, valid);
       const __amdgpu_buffer_rsrc_t rv = tile_rsrc<uint16_t, D>(vp + tile, valid);
-      kr = __builtin_amdgcn_raw_buffer_load_b64(rk, st_ld, 0, kKvLoadPolicy);
-      vr = __builtin_amdgcn_raw_buffer_load_b64(rv, st_ld, 0, kKvLoadPolicy);
+      kr = __builtin_amdgcn_raw_buffer_load_b128(rk, st_ld, 0, kKvLoadPolicy);
+      vr = __builtin_amdgcn_raw_buffer_load_b128(rv, st_ld, 0, kKvLoadPolicy);
     };
-    auto stash = [&](int pg, const u32x2_t& kr, const u32x2_t& vr) {
-      *reinterpret_cast<u32x2_t*>(s_k[pg & 1] + st_off) = kr;
-      *reinterpret_cast<u32x2_t*>(s_v[pg & 1] + st_off) = vr;
+    auto stash = [&](int t, const u32x4& kr, const u32x4& vr) {
+      *reinterpret_cast<u32x4*>(s_k[t & 1] + st_off) = kr;
+      *reinterpret_cast<u32x4*>(s_v[t & 1] + st_off) = vr;
     };
-    auto consume = [&](int pg) {
-      const uint8_t* kt = s_k[pg & 1];
-      const uint8_t* vt = s_v[pg & 1];
-      // S^T = K . Q^T (A: key lane%16, dims 32 st + 8 (lane/16) .. +8), shared by both blocks
-      f32x4_t sc[kPfBlocks];
+    auto consume = [&](int t) {
+      const uint8_t* kt = s_k[t & 1];
+      const uint8_t* vt = s_v[t & 1];
+      const int key0 = t * kPfStep * kPage;  // first key of the step
+      // S^T = K . Q^T per page (A: key lane%16, dims 32 st + 8 (lane/16) .. +8), shared by both blocks
+      f32x4_t sc[kPfBlocks][kPfStep];
 #pragma unroll
-      for (int rb = 0; rb < kPfBlocks; ++rb) sc[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int rb = 0; rb < kPfBlocks; ++rb)
 #pragma unroll
-      for (int st = 0; st < KSTEPS; ++st) {
-        const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + mfma::swz(n, st * 4 + Gq));
+        for (int pp = 0; pp < kPfStep; ++pp) sc[rb][pp] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int rb = 0; rb < kPfBlocks; ++rb)
-          sc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kv),
-                                                           __builtin_bit_cast(bf16x8_t, qt[rb][st]), sc[rb], 0, 0, 0);
-      }
-      // online softmax per block: this lane holds keys 4 (lane/16) + i of its
-      // row; the causal mask applies on the pages that cross the diagonal
-      const bool diag = pg * kPage + kPage - 1 > lim0;
-      float xs[kPfBlocks][4], mc[kPfBlocks];
+      for (int pp = 0; pp < kPfStep; ++pp)
+#pragma unroll
+        for (int st = 0; st < KSTEPS; ++st) {
+          const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + pp * KT + mfma::swz(n, st * 4 + Gq));
+#pragma unroll
+          for (int rb = 0; rb < kPfBlocks; ++rb)
+            sc[rb][pp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, kv), __builtin_bit_cast(bf16x8_t, qt[rb][st]), sc[rb][pp], 0, 0, 0);
+        }
+      // online softmax per block: this lane holds keys key0 + 16 pp + 4 (lane/16) + i
+      // of its row; the causal mask applies on the steps that cross the diagonal
+      const bool diag = key0 + kPfStep * kPage - 1 > lim0;
+      float xs[kPfBlocks][kPfStep * 4], mc[kPfBlocks];
       bool grow = false;
 #pragma unroll
       for (int rb = 0; rb < kPfBlocks; ++rb) {
+        float mx = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          xs[rb][i] = sc[rb][i];
-          if (diag) xs[rb][i] = pg * kPage + Gq * 4 + i <= lim[rb] ? xs[rb][i] : -INFINITY;
-        }
+        for (int pp = 0; pp < kPfStep; ++pp)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float x = sc[rb][pp][i];
+            if (diag) x = key0 + pp * kPage + Gq * 4 + i <= lim[rb] ? x : -INFINITY;
+            xs[rb][pp * 4 + i] = x;
+            mx = fmaxf(mx, x);
+          }
         // scale > 0, so the max commutes with it
-        const float mx = rows4_max(fmaxf(fmaxf(xs[rb][0], xs[rb][1]), fmaxf(xs[rb][2], xs[rb][3]))) * a.scale_log2;
-        mc[rb] = fmaxf(mrow[rb], mx);
+        mc[rb] = fmaxf(mrow[rb], rows4_max(mx) * a.scale_log2);
         grow |= mc[rb] > mrow[rb] + kRescaleSlack;
       }
       if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // rebase every row of the wave
@@ -218,57 +233,73 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
           for (int mb = 0; mb < MB; ++mb) acc[rb][mb] *= alpha;
         }
       }
-      s16x4_t phi[kPfBlocks], plo[kPfBlocks];
+      // P operands: k slots 8 (lane/16) + 4 pp + i hold key 4 (lane/16) + i of page pp
+      mfma::s16x8_t phi[kPfBlocks], plo[kPfBlocks];
 #pragma unroll
       for (int rb = 0; rb < kPfBlocks; ++rb) {
-        float pw[4];
+        s16x4_t h[kPfStep], l[kPfStep];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(xs[rb][i], a.scale_log2, -mrow[rb]));
-        lrow[rb] += (pw[0] + pw[1]) + (pw[2] + pw[3]);
-        mfma::split_hi_lo(pw, phi[rb], plo[rb]);
+        for (int pp = 0; pp < kPfStep; ++pp) {
+          float pw[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(xs[rb][pp * 4 + i], a.scale_log2, -mrow[rb]));
+          lrow[rb] += (pw[0] + pw[1]) + (pw[2] + pw[3]);
+          mfma::split_hi_lo(pw, h[pp], l[pp]);
+        }
+        phi[rb] = __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
+        plo[rb] = __builtin_shufflevector(l[0], l[1], 0, 1, 2, 3, 4, 5, 6, 7);
       }
-      // O^T += V^T . P^T; lane p of group Gq addresses key 4 Gq + p / 4, dims 16 mb + 4 (p % 4)
+      // O^T += V^T . P^T: lane p of group Gq addresses key 4 Gq + p / 4, dims
+      // 16 mb + 4 (p % 4) of each page; the two transposed reads form the A
+      // operand's k slots in the same page-major order as P
       const int vkey = 4 * Gq + (n >> 2);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int d = mb * 16 + 4 * (n & 3);
-        const lds_s16x4_t* src = (const lds_s16x4_t*)(vt + mfma::swz(vkey, d >> 3) + (d & 7) * 2);
-        const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_s16x4_t*>(src));
+        const int off = mfma::swz(vkey, d >> 3) + (d & 7) * 2;
+        const s16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + off));
+        const s16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + KT + off));
+        const bf16x8_t va = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-        for (int rb = 0; rb < kPfBlocks; ++rb) acc[rb][mb] = mfma::pv_mfma(va, phi[rb], plo[rb], acc[rb][mb]);
+        for (int rb = 0; rb < kPfBlocks; ++rb) {
+          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8_t, phi[rb]), acc[rb][mb], 0, 0, 0);
+          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8_t, plo[rb]), acc[rb][mb], 0, 0, 0);
+        }
       }
     };
 
-    // Page p is staged through register set p & 1: page pg + 1 is stored to
-    // LDS while page pg is consumed, and its set is at once refilled with page
-    // pg + 3, so pages pg + 2 and pg + 3 are in flight meanwhile.
-    auto page_barrier = [&](int pg) {
-      __syncthreads();  // page pg is in LDS; everyone is done with page pg - 1
-      if (((pg + 3) & (kPfMaxPages - 1)) == 0 && pg + 3 < npg) {
-        // slide the block-table window to pages pg + 3 .. pg + 3 + kPfMaxPages - 1
-        for (int i = tid; i < min(npg - (pg + 3), kPfMaxPages); i += kPfThreads) s_bt[i] = bt.page(b, pg + 3 + i);
+    // Step t is staged through register set t & 1: step t + 1 is stored to
+    // LDS while step t is consumed, and its set is at once refilled with step
+    // t + 3, so steps t + 2 and t + 3 are in flight meanwhile.
+    auto step_barrier = [&](int t) {
+      __syncthreads();  // step t is in LDS; everyone is done with step t - 1
+      const int pg3 = (t + 3) * kPfStep;  // first page fetched next
+      if ((pg3 & (kPfMaxPages - 1)) == 0 && pg3 < npg) {
+        // slide the block-table window to pages pg3 .. pg3 + kPfMaxPages - 1
+        for (int i = tid; i < min(npg - pg3, kPfMaxPages); i += kPfThreads) s_bt[i] = bt.page(b, pg3 + i);
         __syncthreads();
       }
     };
-    u32x2_t ka, va, kb, vb;
+    u32x4 ka, va, kb, vb;
     // (scheduling barriers keep the issue order the loop's waits assume)
     fetch(0, ka, va);
+    __builtin_amdgcn_sched_barrier(0);
     fetch(1, kb, vb);
     __builtin_amdgcn_sched_barrier(0);
     stash(0, ka, va);
     __builtin_amdgcn_sched_barrier(0);
     fetch(2, ka, va);
     __builtin_amdgcn_sched_barrier(0);
-    // two pages per trip; with npg odd the last trip's second page is null
-    for (int pg = 0; pg < npg; pg += 2) {
-      page_barrier(pg);
-      stash(pg + 1, kb, vb);
-      fetch(pg + 3, kb, vb);
-      consume(pg);
-      page_barrier(pg + 1);
-      stash(pg + 2, ka, va);
-      fetch(pg + 4, ka, va);
-      consume(pg + 1);
+    // two steps per trip; with nst odd the last trip's second step is null
+    for (int t = 0; t < nst; t += 2) {
+      step_barrier(t);
+      stash(t + 1, kb, vb);
+      fetch(t + 3, kb, vb);
+      consume(t);
+      step_barrier(t + 1);
+      stash(t + 2, ka, va);
+      fetch(t + 4, ka, va);
+      consume(t + 1);
     }
 
     // normalise and store straight from the accumulators: lane (n, Gq) holds

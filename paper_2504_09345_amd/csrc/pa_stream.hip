@@ -22,7 +22,8 @@
 // Per workgroup: prefix sums of page counts over all rows (LDS), then a unit
 // table for its range (page id and flags per unit, LDS), then each wave runs
 // a ring of NBUF register tile buffers over the units, exactly as in the
-// split kernel's inner loop.
+// split kernel's inner loop, with a workgroup barrier per unit to keep the
+// waves in step.
 #include "pa_device.h"
 #include "pa_kernels.h"
 #include "pa_tile.h"
@@ -129,6 +130,11 @@ __global__ __launch_bounds__(64 * W) void stream_kernel(StreamArgs a) {
   for (int base = 0; base < n_units; base += NBUF) {
 #pragma unroll
     for (int u = 0; u < NBUF; ++u) {
+      // Lockstep: without a barrier the older wave of each SIMD runs ahead,
+      // waves 0..3 finish ~30% before waves 4..7, and those then stream the
+      // rest alone with half the loads in flight.  In step, the W waves also
+      // issue the W adjacent head tiles of a page together.
+      __syncthreads();
       const int k = base + u;
       int info = 0;
       if (k < n_units) {
