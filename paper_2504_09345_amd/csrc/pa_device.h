@@ -89,6 +89,7 @@ template <int OFF> __device__ __forceinline__ float xor_lanes(float v) {
 // output accumulators need no rescale.  Any base gives the same normalised
 // result, since numerator and denominator share it.
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kRescaleLimit = 256.0f;  // 2^kRescaleSlack
 
 // Max / sum of v over the four 16-lane rows of the wave (lanes l, l ^ 16,
 // l ^ 32, l ^ 48), all lanes ending with the result.  gfx950's row-swap

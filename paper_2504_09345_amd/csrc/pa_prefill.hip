@@ -11,21 +11,25 @@
 // Work item: (sequence, KV head g, block of PB chunk positions).  The block's
 // M = PB * s query rows (position-major, the s heads of group g) are split
 // over 8 waves of two 16-row MFMA blocks each (256 rows), so every operand
-// read from LDS feeds two matrix products.  Per 16-key page:
-//   S^T[key][row] = K . Q^T   (v_mfma_f32_16x16x32_bf16, K as the A operand)
-//   online softmax per row (each lane owns one row and 4 of its keys)
-//   O^T[dim][row] += V^T . P^T (v_mfma_f32_16x16x32_bf16 over 4 keys x the
-//                  bf16 high and low parts of P: fp32-level accuracy)
+// read from LDS feeds two matrix products.  Per step of two 16-key pages:
+//   S^T[key][row] = K . Q^T   (v_mfma_f32_16x16x32_bf16 per page, K as the A
+//                  operand)
+//   online softmax per row (each lane owns one row and 8 of its keys)
+//   O^T[dim][row] += V^T . P^T (two v_mfma_f32_16x16x32_bf16 over the step's
+//                  keys, one with the bf16 high parts of P and one with the
+//                  low parts: fp32-level accuracy)
 // Computing the transposed products keeps "lane l % 16 = query row" in every
 // accumulator, so the softmax statistics, the P operand and the O rescale all
 // stay in the lane that owns the row: no register transposes.
-// The page's K and V tiles are staged in LDS once per workgroup and read by
-// all 8 waves, both with 16-byte chunks XOR-swizzled by key (conflict-free
-// operand reads); each lane's PV operand (4 keys of one dim) is one
-// ds_read_b64_tr_b16 from the naturally ordered V tile.  Staging goes through
-// two register sets, three pages ahead (a set is refilled right after it is
-// stored to LDS), and the item's block-table entries are read from an LDS
-// window, so global latency hides behind two pages of work.
+// The pages' K and V tiles are staged in LDS once per workgroup, two pages
+// per synchronised step, and read by all 8 waves, both with 16-byte chunks
+// XOR-swizzled by key (conflict-free operand reads); each lane's PV operand
+// (4 keys of one dim) is one ds_read_b64_tr_b16 from the [key][dim] V tile.
+// The step loop is software-pipelined: the QK products of step t + 1 are
+// issued before the softmax and PV of step t, so the matrix cores and the
+// VALU work side by side.  Global loads run up to four steps ahead through two
+// register sets and a three-step LDS ring, and the item's block-table
+// entries are read from an LDS window.
 // A persistent grid walks the items in a snake order (item x and 2G-1-x per
 // workgroup) so early and late causal blocks pair up.
 #include "pa_device.h"
@@ -48,6 +52,7 @@ constexpr int kPfBlocks = 2;                       // 16-row MFMA blocks per wav
 constexpr int kPfRows = 16 * kPfBlocks * kPfWaves;  // 256 query rows per item
 constexpr int kPfMaxPages = 2048;                  // block-table window in LDS (power of 2)
 constexpr int kPfStep = 2;                         // pages per synchronised step
+constexpr int kPfLdsSteps = 3;                     // steps staged in LDS at once
 
 }  // namespace
 
@@ -61,8 +66,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   constexpr int C16 = D / 8;            // 16-byte chunks per key
   static_assert(kPfStep * kPage * C16 == kPfThreads, "one 16-byte chunk of K and V per thread and step");
 
-  __shared__ __attribute__((aligned(16))) uint8_t s_k[2][kPfStep * KT];
-  __shared__ __attribute__((aligned(16))) uint8_t s_v[2][kPfStep * KT];
+  __shared__ __attribute__((aligned(16))) uint8_t s_k[kPfLdsSteps][kPfStep * KT];
+  __shared__ __attribute__((aligned(16))) uint8_t s_v[kPfLdsSteps][kPfStep * KT];
   __shared__ int32_t s_bt[kPfMaxPages];
   __shared__ int32_t s_scan[kPfThreads];
   extern __shared__ int32_t s_cum[];  // [B + 1] prefix of items per sequence
@@ -100,6 +105,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   const int st_pg = w / (kPfWaves / kPfStep), st_j = tid % (kPage * C16);
   const int st_key = st_j / C16, st_c = st_j % C16;
   const int st_off = st_pg * KT + mfma::swz(st_key, st_c);
+  const int st_off_v = st_pg * KT + mfma::swz_v(st_key, st_c);
   const int st_ld = st_j * 16;  // byte offset in the global tile
   const int n = lane & 15, Gq = lane >> 4;  // MFMA column (query row of a block) and lane group
 
@@ -140,8 +146,8 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     // this lane's rows: block rb, row m = (w * 2 + rb) * 16 + lane % 16
     u32x4 qt[kPfBlocks][KSTEPS];
     int lim[kPfBlocks];
-    float mrow[kPfBlocks], lrow[kPfBlocks];
-    f32x4_t acc[kPfBlocks][MB];
+    float mrow[kPfBlocks];
+    f32x4_t acc[kPfBlocks][MB], acc_l[kPfBlocks];
 #pragma unroll
     for (int rb = 0; rb < kPfBlocks; ++rb) {
       const int m = (w * kPfBlocks + rb) * 16 + n;
@@ -149,7 +155,7 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       const bool valid = p < npos;
       lim[rb] = valid ? lim0 + p : -1;
       mrow[rb] = kMInit;
-      lrow[rb] = 0.0f;
+      acc_l[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) acc[rb][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       const uint16_t* qrow = qg + ((int64_t)(q0 + pos0 + (valid ? p : 0)) * a.H_q + (int64_t)g * S + h) * D;
@@ -179,15 +185,14 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
       vr = __builtin_amdgcn_raw_buffer_load_b128(rv, st_ld, 0, kKvLoadPolicy);
     };
     auto stash = [&](int t, const u32x4& kr, const u32x4& vr) {
-      *reinterpret_cast<u32x4*>(s_k[t & 1] + st_off) = kr;
-      *reinterpret_cast<u32x4*>(s_v[t & 1] + st_off) = vr;
+      const int buf = t % kPfLdsSteps;
+      *reinterpret_cast<u32x4*>(s_k[buf] + st_off) = kr;
+      *reinterpret_cast<u32x4*>(s_v[buf] + st_off_v) = vr;
     };
-    auto consume = [&](int t) {
-      const uint8_t* kt = s_k[t & 1];
-      const uint8_t* vt = s_v[t & 1];
-      const int key0 = t * kPfStep * kPage;  // first key of the step
-      // S^T = K . Q^T per page (A: key lane%16, dims 32 st + 8 (lane/16) .. +8), shared by both blocks
-      f32x4_t sc[kPfBlocks][kPfStep];
+    // S^T = K . Q^T for the pages of step t (A: key lane%16, dims 32 st +
+    // 8 (lane/16) .. +8), each K read shared by both row blocks
+    auto qk = [&](int t, f32x4_t (&sc)[kPfBlocks][kPfStep]) {
+      const uint8_t* kt = s_k[t % kPfLdsSteps];
 #pragma unroll
       for (int rb = 0; rb < kPfBlocks; ++rb)
 #pragma unroll
@@ -202,81 +207,113 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
             sc[rb][pp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                 __builtin_bit_cast(bf16x8_t, kv), __builtin_bit_cast(bf16x8_t, qt[rb][st]), sc[rb][pp], 0, 0, 0);
         }
-      // online softmax per block: this lane holds keys key0 + 16 pp + 4 (lane/16) + i
-      // of its row; the causal mask applies on the steps that cross the diagonal
-      const bool diag = key0 + kPfStep * kPage - 1 > lim0;
-      float xs[kPfBlocks][kPfStep * 4], mc[kPfBlocks];
-      bool grow = false;
+    };
+    // online softmax of step t's scores and O^T += V^T . P^T.  Row sums come
+    // from the matrix cores too: acc_l += ones . P^T (every entry of a lane's
+    // acc_l holds its row's sum).
+    const bf16x8_t ones = __builtin_bit_cast(
+        bf16x8_t, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+    auto softmax_pv = [&](int t, const f32x4_t (&sc)[kPfBlocks][kPfStep]) {
+      const uint8_t* vt = s_v[t % kPfLdsSteps];
+      const int key0 = t * kPfStep * kPage;  // first key of the step
+      // this lane holds keys key0 + 16 pp + 4 (lane/16) + i of its row; the
+      // causal mask applies on the steps that cross the diagonal
+      float xs[kPfBlocks][kPfStep * 4];
+      if (key0 + kPfStep * kPage - 1 > lim0) {
 #pragma unroll
-      for (int rb = 0; rb < kPfBlocks; ++rb) {
-        float mx = -INFINITY;
+        for (int rb = 0; rb < kPfBlocks; ++rb)
 #pragma unroll
-        for (int pp = 0; pp < kPfStep; ++pp)
+          for (int pp = 0; pp < kPfStep; ++pp)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float x = sc[rb][pp][i];
-            if (diag) x = key0 + pp * kPage + Gq * 4 + i <= lim[rb] ? x : -INFINITY;
-            xs[rb][pp * 4 + i] = x;
-            mx = fmaxf(mx, x);
-          }
-        // scale > 0, so the max commutes with it
-        mc[rb] = fmaxf(mrow[rb], rows4_max(mx) * a.scale_log2);
-        grow |= mc[rb] > mrow[rb] + kRescaleSlack;
+            for (int i = 0; i < 4; ++i)
+              xs[rb][pp * 4 + i] = key0 + pp * kPage + Gq * 4 + i <= lim[rb] ? sc[rb][pp][i] : -INFINITY;
+      } else {
+#pragma unroll
+        for (int rb = 0; rb < kPfBlocks; ++rb)
+#pragma unroll
+          for (int pp = 0; pp < kPfStep; ++pp)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xs[rb][pp * 4 + i] = sc[rb][pp][i];
       }
-      if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // rebase every row of the wave
+      // weights against the current base; the base only moves when one of
+      // them exceeds 2^kRescaleSlack (or is the first finite score of a row,
+      // whose base is still kMInit: the weight is then +inf)
+      float pw[kPfBlocks][kPfStep * 4];
+      auto weights = [&]() {
+        bool big = false;
 #pragma unroll
         for (int rb = 0; rb < kPfBlocks; ++rb) {
-          const float alpha = fast_exp2(mrow[rb] - mc[rb]);
-          mrow[rb] = mc[rb];
-          lrow[rb] *= alpha;
+          float pmax = 0.0f;
+#pragma unroll
+          for (int j = 0; j < kPfStep * 4; ++j) {
+            pw[rb][j] = fast_exp2(fmaf(xs[rb][j], a.scale_log2, -mrow[rb]));
+            pmax = fmaxf(pmax, pw[rb][j]);
+          }
+          big |= pmax > kRescaleLimit;
+        }
+        return big;
+      };
+      if (__builtin_amdgcn_ballot_w64(weights()) != 0) {  // rebase every row of the wave
+#pragma unroll
+        for (int rb = 0; rb < kPfBlocks; ++rb) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int j = 0; j < kPfStep * 4; ++j) mx = fmaxf(mx, xs[rb][j]);
+          // scale > 0, so the max commutes with it
+          const float mc = fmaxf(mrow[rb], rows4_max(mx) * a.scale_log2);
+          const float alpha = fast_exp2(mrow[rb] - mc);
+          mrow[rb] = mc;
+          acc_l[rb] *= alpha;
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb) acc[rb][mb] *= alpha;
         }
+        weights();
       }
       // P operands: k slots 8 (lane/16) + 4 pp + i hold key 4 (lane/16) + i of page pp
-      mfma::s16x8_t phi[kPfBlocks], plo[kPfBlocks];
+      bf16x8_t phi[kPfBlocks], plo[kPfBlocks];
 #pragma unroll
       for (int rb = 0; rb < kPfBlocks; ++rb) {
         s16x4_t h[kPfStep], l[kPfStep];
 #pragma unroll
         for (int pp = 0; pp < kPfStep; ++pp) {
-          float pw[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(xs[rb][pp * 4 + i], a.scale_log2, -mrow[rb]));
-          lrow[rb] += (pw[0] + pw[1]) + (pw[2] + pw[3]);
-          mfma::split_hi_lo(pw, h[pp], l[pp]);
+          const float q4[4] = {pw[rb][pp * 4], pw[rb][pp * 4 + 1], pw[rb][pp * 4 + 2], pw[rb][pp * 4 + 3]};
+          mfma::split_hi_lo(q4, h[pp], l[pp]);
         }
-        phi[rb] = __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
-        plo[rb] = __builtin_shufflevector(l[0], l[1], 0, 1, 2, 3, 4, 5, 6, 7);
+        phi[rb] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        plo[rb] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(l[0], l[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, phi[rb], acc_l[rb], 0, 0, 0);
+        acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, plo[rb], acc_l[rb], 0, 0, 0);
       }
-      // O^T += V^T . P^T: lane p of group Gq addresses key 4 Gq + p / 4, dims
-      // 16 mb + 4 (p % 4) of each page; the two transposed reads form the A
-      // operand's k slots in the same page-major order as P
+      // lane p of group Gq addresses key 4 Gq + p / 4, dims 16 mb + 4 (p % 4)
+      // of each page; the two transposed reads form the A operand's k slots in
+      // the same page-major order as P
       const int vkey = 4 * Gq + (n >> 2);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int d = mb * 16 + 4 * (n & 3);
-        const int off = mfma::swz(vkey, d >> 3) + (d & 7) * 2;
+        const int off = mfma::swz_v(vkey, d >> 3) + (d & 7) * 2;
         const s16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + off));
         const s16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + KT + off));
         const bf16x8_t va = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
         for (int rb = 0; rb < kPfBlocks; ++rb) {
-          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8_t, phi[rb]), acc[rb][mb], 0, 0, 0);
-          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, __builtin_bit_cast(bf16x8_t, plo[rb]), acc[rb][mb], 0, 0, 0);
+          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[rb], acc[rb][mb], 0, 0, 0);
+          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[rb], acc[rb][mb], 0, 0, 0);
         }
       }
     };
 
-    // Step t is staged through register set t & 1: step t + 1 is stored to
-    // LDS while step t is consumed, and its set is at once refilled with step
-    // t + 3, so steps t + 2 and t + 3 are in flight meanwhile.
+    // Pipeline.  Step t is staged through register set t & 1 and LDS buffer
+    // t % 3.  Iteration t stores step t + 2 to LDS and refills its register
+    // set with step t + 4 (steps t + 3 and t + 4 in flight), issues the QK
+    // products of step t + 1 and then runs the softmax and PV of step t, so
+    // the matrix cores work on QK(t + 1) while the VALU does softmax(t).
     auto step_barrier = [&](int t) {
-      __syncthreads();  // step t is in LDS; everyone is done with step t - 1
-      const int pg3 = (t + 3) * kPfStep;  // first page fetched next
-      if ((pg3 & (kPfMaxPages - 1)) == 0 && pg3 < npg) {
-        // slide the block-table window to pages pg3 .. pg3 + kPfMaxPages - 1
-        for (int i = tid; i < min(npg - pg3, kPfMaxPages); i += kPfThreads) s_bt[i] = bt.page(b, pg3 + i);
+      __syncthreads();  // steps t, t + 1 are in LDS; everyone is done with step t - 1
+      const int pgf = (t + 4) * kPfStep;  // first page fetched next
+      if ((pgf & (kPfMaxPages - 1)) == 0 && pgf < npg) {
+        // slide the block-table window to pages pgf .. pgf + kPfMaxPages - 1
+        for (int i = tid; i < min(npg - pgf, kPfMaxPages); i += kPfThreads) s_bt[i] = bt.page(b, pgf + i);
         __syncthreads();
       }
     };
@@ -290,25 +327,33 @@ __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     fetch(2, ka, va);
     __builtin_amdgcn_sched_barrier(0);
+    stash(1, kb, vb);
+    __builtin_amdgcn_sched_barrier(0);
+    fetch(3, kb, vb);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();  // steps 0 and 1 are in LDS
+    f32x4_t sc[kPfBlocks][kPfStep], sn[kPfBlocks][kPfStep];
+    qk(0, sc);
     // two steps per trip; with nst odd the last trip's second step is null
     for (int t = 0; t < nst; t += 2) {
       step_barrier(t);
-      stash(t + 1, kb, vb);
-      fetch(t + 3, kb, vb);
-      consume(t);
-      step_barrier(t + 1);
       stash(t + 2, ka, va);
       fetch(t + 4, ka, va);
-      consume(t + 1);
+      qk(t + 1, sn);
+      softmax_pv(t, sc);
+      step_barrier(t + 1);
+      stash(t + 3, kb, vb);
+      fetch(t + 5, kb, vb);
+      qk(t + 2, sc);
+      softmax_pv(t + 1, sn);
     }
 
     // normalise and store straight from the accumulators: lane (n, Gq) holds
     // dims 16 mb + 4 Gq + i of row (w * 2 + rb) * 16 + n
 #pragma unroll
     for (int rb = 0; rb < kPfBlocks; ++rb) {
-      const float l = rows4_sum(lrow[rb]);
       if (lim[rb] >= 0) {
-        const float inv = 1.0f / l;
+        const float inv = 1.0f / acc_l[rb][0];
         const int m = (w * kPfBlocks + rb) * 16 + n;
         const int p = m / S, h = m - p * S;
         uint16_t* orow = og + ((int64_t)(q0 + pos0 + p) * a.H_q + (int64_t)g * S + h) * D;

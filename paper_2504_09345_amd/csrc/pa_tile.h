@@ -274,8 +274,8 @@ __device__ __forceinline__ void partial_rows(const DecodeState<T, D, S>& st, int
 //                                the k dimension holds 4 tokens x {hi, lo})
 // Lane l owns head column l % 16 and tokens 4 (l / 16) .. +3 of every tile, so
 // the softmax state and the rescale stay in the lane.  The wave stages each
-// tile through its own 8 KiB of LDS: K with 16-byte chunks XOR-swizzled by
-// token (conflict-free operand reads), V in natural order, read back as the
+// tile through its own 8 KiB of LDS, K and V with 16-byte chunks XOR-swizzled
+// by token (conflict-free operand reads), V read back as the
 // transposed PV operand with ds_read_b64_tr_b16 (lane j of a 16-lane group
 // receives element j % 4 of the 8-byte blocks addressed by lanes j / 4 + 4 i).
 namespace mfma {
@@ -289,7 +289,13 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 constexpr int kD = 128;
 constexpr int kTile = kPage * kD * 2;  // 4 KiB
 
+// Byte offset of 16-byte chunk `chunk` of key `key` in a staged [16][kD] bf16
+// tile.  K: chunks XOR-ed with the key, so the 16 lanes of a QK operand read
+// (16 keys, one chunk each) hit 16 distinct bank groups.  V: chunks XOR-ed
+// with 2 (key mod 8), so a transposed PV read (per half wave: 8 keys x 2
+// adjacent chunks) also hits 16 distinct 16-byte bank groups.
 __device__ __forceinline__ int swz(int key, int chunk) { return key * (kD * 2) + ((chunk ^ (key & 15)) << 4); }
+__device__ __forceinline__ int swz_v(int key, int chunk) { return key * (kD * 2) + ((chunk ^ ((key & 7) << 1)) << 4); }
 
 template <int S>
 struct State {
@@ -349,7 +355,7 @@ __device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u3
   for (int i = 0; i < 4; ++i) {
     const int tok = G + 4 * i;
     *reinterpret_cast<u32x4*>(lds + swz(tok, p)) = k[i];
-    *reinterpret_cast<u32x4*>(lds + kTile + swz(tok, p)) = v[i];
+    *reinterpret_cast<u32x4*>(lds + kTile + swz_v(tok, p)) = v[i];
   }
   // S^T = K . Q^T
   f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -388,7 +394,7 @@ __device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u3
 #pragma unroll
   for (int mb = 0; mb < kD / 16; ++mb) {
     const int d = mb * 16 + 4 * (p & 3);
-    const lds_s16x4_t* src = (const lds_s16x4_t*)(lds + kTile + swz(vtok, d >> 3) + (d & 7) * 2);
+    const lds_s16x4_t* src = (const lds_s16x4_t*)(lds + kTile + swz_v(vtok, d >> 3) + (d & 7) * 2);
     const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_s16x4_t*>(src));
     st.acc[mb] = pv_mfma(va, phi, plo, st.acc[mb]);
   }
