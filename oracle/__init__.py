@@ -54,6 +54,8 @@ def _bind(lib):
                                            I32, ctypes.c_float, I32, I32, I32, ctypes.c_int64,
                                            I32, P]
     lib.oracle_softmax_weights.restype = ctypes.c_int
+    lib.oracle_kv_append.argtypes = [P, P, I32, P, I32, P, P, I32, I32, I32, I32, I32, P, P]
+    lib.oracle_kv_append.restype = ctypes.c_int
     lib.oracle_set_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_threads.restype = None
     lib.oracle_get_threads.argtypes = []
@@ -163,3 +165,27 @@ def softmax_weights(q, k_pages, block_table, context_lens, scale, b, h, L=1, r=0
     if rc < 0:
         raise ValueError(f"oracle_softmax_weights failed with code {rc}")
     return w[:rc]
+
+
+def kv_append(k_new, v_new, block_table, context_lens, k_pages, v_pages, query_start_loc=None):
+    """New pools after storing the new tokens' K/V (rows of k_new / v_new,
+    [T][H_kv][D]) at the last positions of each sequence's context.
+
+    query_start_loc=None is the decode layout (row b, position context_lens[b]-1).
+    The input pools are not modified; updated copies are returned.
+    """
+    k_new, v_new = _c(k_new), _c(v_new)
+    if k_new.dtype != v_new.dtype or k_new.shape != v_new.shape:
+        raise ValueError("k_new and v_new must match")
+    kp, vp = np.array(k_pages, copy=True, order="C"), np.array(v_pages, copy=True, order="C")
+    if kp.dtype != k_new.dtype or vp.dtype != k_new.dtype:
+        raise ValueError("pool and new rows must share the element type")
+    bt, cl = _c(block_table, np.int32), _c(context_lens, np.int32)
+    qsl = None if query_start_loc is None else _c(query_start_loc, np.int32)
+    N, H_kv, P, D = kp.shape
+    rc = _load().oracle_kv_append(_ptr(k_new), _ptr(v_new), k_new.dtype.itemsize, _ptr(bt),
+                                  bt.shape[1], _ptr(cl), None if qsl is None else _ptr(qsl),
+                                  cl.shape[0], H_kv, D, P, N, _ptr(kp), _ptr(vp))
+    if rc != 0:
+        raise ValueError(f"oracle_kv_append failed with code {rc}")
+    return kp, vp

@@ -292,3 +292,67 @@ int oracle_softmax_weights(const void *q, const void *k_pages, int dtype,
   for (int32_t t = 0; t < n_vis; ++t) w_out[t] = w_out[t] / l;
   return n_vis;
 }
+
+/* KV append: the step right before attention.  The new tokens' keys and values
+ * are stored into the paged cache, and attention then runs over the cache
+ * (Sec. 6.4: the task that receives a decode token's pre-attention K/V stores
+ * it in the KV cache before it attends).
+ *
+ * Sequence b appends L_b tokens, which are the last L_b positions of its
+ * context: with query_start_loc, row query_start_loc[b] + j (j < L_b) holds
+ * position context_lens[b] - L_b + j; without it (decode), row b holds position
+ * context_lens[b] - 1, and a sequence with context 0 appends nothing.  For each
+ * such row and kv head g, the D elements k_new[row][g][.] and v_new[row][g][.]
+ * are copied bit for bit into kv head g of slot (position % P) of page
+ * block_table[b][position / P].  Nothing else in the pools changes.
+ *   k_new, v_new      [T][H_kv][D], elements of elem_bytes bytes (2: bf16, 4: fp32)
+ *   k_pages, v_pages  [num_pages][H_kv][P][D], updated in place
+ * Returns 0, or -1 (null pointer, bad sizes, L_b > context_lens[b], row offsets
+ * not monotone, or a written position whose page entry is outside the pool or
+ * the table row); on -1 the pools are unchanged. */
+int oracle_kv_append(const void *k_new, const void *v_new, int32_t elem_bytes,
+                     const int32_t *block_table, int32_t max_pages_per_seq,
+                     const int32_t *context_lens, const int32_t *query_start_loc, int32_t B,
+                     int32_t H_kv, int32_t D, int32_t P, int32_t num_pages, void *k_pages,
+                     void *v_pages) {
+  if (!k_new || !v_new || !block_table || !context_lens || !k_pages || !v_pages) return -1;
+  if (elem_bytes != 2 && elem_bytes != 4) return -1;
+  if (B < 0 || H_kv <= 0 || D <= 0 || P <= 0 || num_pages < 0 || max_pages_per_seq < 0) return -1;
+  if (query_start_loc && B > 0 && query_start_loc[0] != 0) return -1;
+  /* validate everything first, so that a failure leaves the pools unchanged */
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t C = context_lens[b];
+    int32_t L;
+    if (query_start_loc) {
+      L = query_start_loc[b + 1] - query_start_loc[b];
+      if (L < 0) return -1;
+    } else {
+      L = C > 0 ? 1 : 0;
+    }
+    if (C < 0 || L > C) return -1;
+    for (int32_t j = 0; j < L; ++j) {
+      const int32_t pos = C - L + j;
+      if (pos / P >= max_pages_per_seq) return -1;
+      const int32_t page = block_table[(int64_t)b * max_pages_per_seq + pos / P];
+      if (page < 0 || page >= num_pages) return -1;
+    }
+  }
+  const size_t row_bytes = (size_t)D * (size_t)elem_bytes;
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t C = context_lens[b];
+    const int32_t L = query_start_loc ? query_start_loc[b + 1] - query_start_loc[b] : (C > 0 ? 1 : 0);
+    const int64_t row0 = query_start_loc ? query_start_loc[b] : b;
+    for (int32_t j = 0; j < L; ++j) {
+      const int32_t pos = C - L + j;
+      const int32_t page = block_table[(int64_t)b * max_pages_per_seq + pos / P];
+      const int32_t slot = pos % P;
+      for (int32_t g = 0; g < H_kv; ++g) {
+        const size_t src = ((size_t)(row0 + j) * H_kv + g) * row_bytes;
+        const size_t dst = (((size_t)page * H_kv + g) * P + slot) * row_bytes;
+        memcpy((char *)k_pages + dst, (const char *)k_new + src, row_bytes);
+        memcpy((char *)v_pages + dst, (const char *)v_new + src, row_bytes);
+      }
+    }
+  }
+  return 0;
+}

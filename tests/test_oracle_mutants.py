@@ -40,6 +40,14 @@ MUTANTS = [
      "rows_out[n++] = (int64_t)page * P + t / P;"),
     ("weights_not_normalised", "for (int32_t t = 0; t < n_vis; ++t) w_out[t] = w_out[t] / l;",
      "for (int32_t t = 0; t < n_vis; ++t) w_out[t] = w_out[t];"),
+    ("append_position_one_late", "const int32_t pos = C - L + j;\n      const int32_t page",
+     "const int32_t pos = C - L + j + 1;\n      const int32_t page"),
+    ("append_head_layout", "const size_t dst = (((size_t)page * H_kv + g) * P + slot) * row_bytes;",
+     "const size_t dst = (((size_t)page * P + slot) * H_kv + g) * row_bytes;"),
+    ("append_rows_reversed", "const size_t src = ((size_t)(row0 + j) * H_kv + g) * row_bytes;",
+     "const size_t src = ((size_t)(row0 + L - 1 - j) * H_kv + g) * row_bytes;"),
+    ("append_v_from_k", "(const char *)v_new + src", "(const char *)k_new + src"),
+    ("append_decode_skips_nothing", "L = C > 0 ? 1 : 0;\n    }", "L = 1;\n    }"),
 ]
 
 

@@ -250,8 +250,8 @@ def test_poisoned_pool_does_not_leak():
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
 
 
-def _read_gather_fixture():
-    path = os.path.join(GOLDEN, "gather_tiny.txt")
+def _read_gather_fixture(path):
+    """Sections of integer rows from a hand-derived fixture under tests/golden."""
     sec, data = None, {}
     with open(path) as f:
         for line in f:
@@ -267,7 +267,7 @@ def _read_gather_fixture():
 
 
 def test_gather_indices_hand_fixture():
-    fx = _read_gather_fixture()
+    fx = _read_gather_fixture(os.path.join(GOLDEN, "gather_tiny.txt"))
     bt = np.array(fx["block_table"], np.int32)
     ctx = np.array(fx["context_lens"][0], np.int32)
     rows = oracle.gather_indices(bt, ctx, 16, int(fx["num_pages"][0][0]))
@@ -305,3 +305,100 @@ def test_oracle_thread_count_does_not_change_result():
     b = _run_oracle(batch)
     oracle.set_threads(0)
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+# --- KV append: the cache write before attention -----------------------------
+
+def _kv_rows(T, H_kv, D, dtype=np.uint16):
+    """Row r, kv head g holds (100 r + 10 g + 1, 100 r + 10 g + 2, ...)."""
+    r = np.arange(T)[:, None, None]
+    g = np.arange(H_kv)[None, :, None]
+    d = np.arange(D)[None, None, :]
+    k = (100 * r + 10 * g + 1 + d).astype(dtype)
+    return k, (k + 1000).astype(dtype)
+
+
+@pytest.mark.parametrize("layout", ["varlen", "decode"])
+def test_kv_append_hand_fixture(layout):
+    fx = _read_gather_fixture(os.path.join(GOLDEN, "kv_append_tiny.txt"))
+    bt = np.array(fx["block_table"], np.int32)
+    ctx = np.array(fx["context_lens"][0], np.int32)
+    N, H_kv, P, D = int(fx["num_pages"][0][0]), 2, 4, 2
+    qsl = np.array(fx["query_start_loc"][0], np.int32) if layout == "varlen" else None
+    T = int(qsl[-1]) if layout == "varlen" else len(ctx)
+    kn, vn = _kv_rows(T, H_kv, D)
+    kp = np.full((N, H_kv, P, D), 7, np.uint16)
+    vp = np.full((N, H_kv, P, D), 9, np.uint16)
+    k2, v2 = oracle.kv_append(kn, vn, bt, ctx, kp, vp, query_start_loc=qsl)
+    ek, ev = kp.copy(), vp.copy()
+    for row, page, slot in fx[f"{layout}_writes"]:
+        ek[page, :, slot, :] = kn[row]
+        ev[page, :, slot, :] = vn[row]
+    assert np.array_equal(k2, ek) and np.array_equal(v2, ev)
+    assert np.array_equal(kp, np.full_like(kp, 7))  # inputs untouched
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_kv_append_lands_where_the_gather_reads(dtype):
+    """After the append, the gather (an independent oracle function) finds the
+    new rows at each sequence's last positions; every other pool row is
+    unchanged."""
+    b = W.generate("mixed", seed=5, dtype=dtype, overrides=dict(
+        prefill=(3, 40, 0, 70), decode=(5, 1, 90), H_q=8, H_kv=2, D=64))
+    qsl, ctx = b.query_start_loc, b.context_lens
+    T, H_kv, D = int(qsl[-1]), b.num_kv_heads, b.head_dim
+    rng = np.random.default_rng(11)
+    mk = (lambda shape: rng.integers(0, 1 << 16, shape, dtype=np.uint16)) if dtype == "bf16" else \
+        (lambda shape: rng.standard_normal(shape).astype(np.float32))
+    kn, vn = mk((T, H_kv, D)), mk((T, H_kv, D))
+    k2, v2 = oracle.kv_append(kn, vn, b.block_table, ctx, b.k_pages, b.v_pages, query_start_loc=qsl)
+    rows = oracle.gather_indices(b.block_table, ctx, 16, b.num_pages)
+    starts = np.concatenate([[0], np.cumsum(ctx)])
+    flat = lambda a: a.transpose(0, 2, 1, 3).reshape(-1, H_kv, D)
+    new_rows = []
+    for s in range(b.num_seqs):
+        L = int(qsl[s + 1] - qsl[s])
+        for j in range(L):
+            fr = rows[starts[s] + ctx[s] - L + j]
+            new_rows.append(fr)
+            assert np.array_equal(flat(k2)[fr], kn[qsl[s] + j])
+            assert np.array_equal(flat(v2)[fr], vn[qsl[s] + j])
+    keep = np.setdiff1d(np.arange(flat(k2).shape[0]), new_rows)
+    assert np.array_equal(flat(k2)[keep], flat(b.k_pages)[keep])
+    assert np.array_equal(flat(v2)[keep], flat(b.v_pages)[keep])
+
+
+def test_kv_append_restores_the_cache_attention_reads():
+    """Poison each sequence's last cached token, append its original K/V as
+    the decode token: the pool is restored bit for bit, and so is attention."""
+    b = W.generate("tiny", seed=6)
+    rows = oracle.gather_indices(b.block_table, b.context_lens, 16, b.num_pages)
+    starts = np.concatenate([[0], np.cumsum(b.context_lens)])
+    last = rows[starts[1:] - 1]
+    H_kv, D = b.num_kv_heads, b.head_dim
+    flat = lambda a: a.transpose(0, 2, 1, 3).reshape(-1, H_kv, D)
+    kn, vn = flat(b.k_pages)[last].copy(), flat(b.v_pages)[last].copy()
+    kp, vp = b.k_pages.copy(), b.v_pages.copy()
+    kp[last // 16, :, last % 16, :] = 0x7FC0  # NaN
+    vp[last // 16, :, last % 16, :] = 0x7FC0
+    assert np.isnan(W.bf16_bits_to_f32(kp)).any()
+    k2, v2 = oracle.kv_append(kn, vn, b.block_table, b.context_lens, kp, vp)
+    assert np.array_equal(k2, b.k_pages) and np.array_equal(v2, b.v_pages)
+    ref = oracle.paged_attn(b.q, b.k_pages, b.v_pages, b.block_table, b.context_lens, b.scale)
+    got = oracle.paged_attn(b.q, k2, v2, b.block_table, b.context_lens, b.scale)
+    assert np.array_equal(ref, got)
+
+
+def test_kv_append_rejects_bad_inputs_and_leaves_pools_unchanged():
+    b = W.generate("tiny", seed=7)
+    kn = np.zeros((b.num_seqs, b.num_kv_heads, b.head_dim), np.uint16)
+    bt = b.block_table.copy()
+    c = int(b.context_lens[0]) - 1
+    bt[0, c // 16] = b.num_pages  # the page of seq 0's new token is outside the pool
+    with pytest.raises(ValueError):
+        oracle.kv_append(kn, kn, bt, b.context_lens, b.k_pages, b.v_pages)
+    qsl = np.array([0, 1, 1 + int(b.context_lens[1]) + 1, 0, 0], np.int32)  # L > ctx for seq 1
+    qsl[3:] = qsl[2]
+    kq = np.zeros((int(qsl[-1]), b.num_kv_heads, b.head_dim), np.uint16)
+    with pytest.raises(ValueError):
+        oracle.kv_append(kq, kq, b.block_table, b.context_lens, b.k_pages, b.v_pages, query_start_loc=qsl)
