@@ -73,6 +73,14 @@ def algorithmic_bytes(b: W.Batch) -> dict:
     return dict(kv=kv, q_out=qo, meta=meta, total=kv + qo + meta)
 
 
+def append_bytes(b: W.Batch) -> int:
+    """KV append: every new token's K and V vectors (all KV heads) read from
+    the new-row arrays and written into the pool once.  Rows = the chunk and
+    decode rows of a varlen batch, one per non-empty sequence in decode."""
+    rows = b.num_q_rows if b.query_start_loc is not None else int((b.context_lens > 0).sum())
+    return 2 * 2 * rows * b.num_kv_heads * b.head_dim * elem_bytes(b.dtype)
+
+
 def algorithmic_flops(b: W.Batch) -> int:
     """QK (2D) and PV (2D) per query head per visible key."""
     ql = b.q_lens.astype(np.int64)
@@ -174,6 +182,9 @@ def main():
     ap.add_argument("--pages-per-split", type=int, default=0)
     ap.add_argument("--rotate", type=int, default=0,
                     help="pool copies to rotate through (0: enough for >= 1.5 GB per copy set)")
+    ap.add_argument("--append", action="store_true",
+                    help="each step first stores the step's new tokens' K/V into the cache "
+                         "(pa_kv_append), then attends")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -220,8 +231,27 @@ def main():
     K, Wm = args.steps, args.warmup
     marks = [pb.PaTiming(ev.create(), ev.create(), ev.create()) for _ in range(K)]
 
+    if args.append:
+        rows_new = dev_q.shape[0]
+        rng = np.random.default_rng(args.seed + 1000)
+        new_kv = [to_device(W.f32_to_bf16_bits(
+            (rng.standard_normal((rows_new, batch.num_kv_heads, batch.head_dim)) * 0.5).astype(np.float32))
+            if batch.dtype == "bf16" else
+            (rng.standard_normal((rows_new, batch.num_kv_heads, batch.head_dim)) * 0.5).astype(np.float32),
+            torch) for _ in range(2)]
+    app_marks = []
+
     def step(i, timing=None):
         k, v = pools[i % R]
+        if args.append:
+            if timing is not None:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            pb.pa_kv_append(new_kv[0], new_kv[1], bt, cl, k, v, dims, query_start_loc=qsl,
+                            stream=stream)
+            if timing is not None:
+                e1.record(stream)
+                app_marks.append((e0, e1))
         if qsl is None:
             pb.paged_attn(dev_q, k, v, bt, cl, batch.scale, out, dims, ws, stream, timing)
         else:
@@ -258,6 +288,13 @@ def main():
     for m in marks:
         ev.destroy(m.attn_begin), ev.destroy(m.attn_end), ev.destroy(m.reduce_end)
 
+    append = None
+    if args.append:
+        app_us = [a.elapsed_time(b_) * 1e3 for a, b_ in app_marks]
+        ab = append_bytes(batch)
+        append = {"kernel_us_mean": round(float(np.mean(app_us)), 2),
+                  "bytes": ab, "gb_per_s": round(ab / (float(np.mean(app_us)) / 1e6) / 1e9, 1),
+                  "frac_of_hbm_peak": round(ab / (float(np.mean(app_us)) / 1e6) / 1e9 / HBM_PEAK_GBPS, 4)}
     by = algorithmic_bytes(batch)
     traffic, traffic_src = measured_traffic(args.workload) if args.pages_per_split == 0 else (None, None)
     fl = algorithmic_flops(batch)
@@ -285,6 +322,7 @@ def main():
             "num_kv_heads": batch.num_kv_heads, "head_dim": batch.head_dim, "page_size": 16,
             "context_len_total": int(batch.context_lens.sum()),
             "pages_per_split": args.pages_per_split, "seed": args.seed, "pool_copies": R,
+            "kv_append": bool(args.append),
         },
         "roofline": {
             "bound": "hbm",
@@ -308,6 +346,8 @@ def main():
         },
         "gen_s": round(gen_s, 1),
     }
+    if append is not None:
+        res["kernels"]["kv_append"] = append
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = _cpu_baseline(batch, args.cpu_baseline_seconds, None)
         res["cpu_baseline"]["host_cpu"] = _cpu_model()

@@ -166,6 +166,34 @@ int pa_gather_trace(const int32_t *block_table, const int32_t *context_lens,
                     const int64_t *row_start, const pa_dims_t *dims, int64_t *rows_out,
                     hipStream_t stream);
 
+/* KV append: store the new tokens' keys and values into the paged cache, the
+ * step right before attention (Sec. 6.4: the task that receives a decode
+ * token's pre-attention K/V stores it in the KV cache, then attends; Sec. 5.5
+ * paging).  Sequence b appends L_b tokens at the LAST L_b positions of its
+ * context, so context_lens already counts them (the same convention as the
+ * attention calls):
+ *   - query_start_loc != NULL: rows query_start_loc[b] .. query_start_loc[b+1]-1,
+ *     row query_start_loc[b] + j at position context_lens[b] - L_b + j;
+ *     dims->num_q_rows rows in total;
+ *   - query_start_loc == NULL (decode): row b at position context_lens[b] - 1,
+ *     nothing for context_lens[b] = 0; dims->num_seqs rows.
+ * Row r, KV head g (D elements) is copied bit for bit into KV head g of slot
+ * position % page_size of page block_table[b][position / page_size].
+ *   k_new, v_new     [rows][num_kv_heads][head_dim]   device, read
+ *   k_pages, v_pages pool, see layouts above         device, updated in place
+ *   block_table, context_lens, query_start_loc       device, read
+ * Uses num_seqs, num_kv_heads, head_dim, page_size, num_pages,
+ * max_pages_per_seq, max_context_len, dtype and (varlen) num_q_rows of dims.
+ * A sequence whose chunk is longer than its context, whose context exceeds
+ * max_context_len, or whose written page entry lies outside [0, num_pages) is
+ * not written (nothing outside the pool is ever touched).  Rows of different
+ * calls on one stream are written in call order; the caller runs attention on
+ * the same stream after this call.
+ * Errors: PA_EINVAL, PA_ENOTSUP, PA_EHIP. */
+int pa_kv_append(const void *k_new, const void *v_new, const int32_t *block_table,
+                 const int32_t *context_lens, const int32_t *query_start_loc, void *k_pages,
+                 void *v_pages, const pa_dims_t *dims, hipStream_t stream);
+
 /* Static description of an error code (never NULL). */
 const char *pa_strerror(int code);
 

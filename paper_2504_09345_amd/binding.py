@@ -21,7 +21,7 @@ PA_BF16, PA_FP32 = 0, 1
 PAGE_SIZE = 16
 
 EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "pa_gather_trace",
-            "pa_strerror")
+            "pa_kv_append", "pa_strerror")
 
 
 class PaDims(ctypes.Structure):
@@ -65,6 +65,8 @@ def load():
     lib.paged_attn_varlen.restype = ctypes.c_int
     lib.pa_gather_trace.argtypes = [P, P, P, DP, P, P]
     lib.pa_gather_trace.restype = ctypes.c_int
+    lib.pa_kv_append.argtypes = [P, P, P, P, P, P, P, DP, P]
+    lib.pa_kv_append.restype = ctypes.c_int
     lib.pa_strerror.argtypes = [ctypes.c_int]
     lib.pa_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -168,4 +170,15 @@ def pa_gather_trace(block_table, context_lens, row_start, dims: PaDims, rows_out
                                 ctypes.byref(dims), _addr(rows_out), _stream(stream))
     if check and rc != PA_OK:
         raise PagedAttnError("pa_gather_trace", rc)
+    return rc
+
+
+def pa_kv_append(k_new, v_new, block_table, context_lens, k_pages, v_pages, dims: PaDims,
+                 query_start_loc=None, stream=None, check=True) -> int:
+    """int pa_kv_append(...): store the new tokens' K/V into the paged pools."""
+    rc = load().pa_kv_append(_addr(k_new), _addr(v_new), _addr(block_table), _addr(context_lens),
+                             _addr(query_start_loc), _addr(k_pages), _addr(v_pages),
+                             ctypes.byref(dims), _stream(stream))
+    if check and rc != PA_OK:
+        raise PagedAttnError("pa_kv_append", rc)
     return rc

@@ -296,6 +296,47 @@ int pa_gather_trace(const int32_t* block_table, const int32_t* context_lens,
   return e == hipSuccess ? PA_OK : PA_EHIP;
 }
 
+int pa_kv_append(const void* k_new, const void* v_new, const int32_t* block_table,
+                 const int32_t* context_lens, const int32_t* query_start_loc, void* k_pages,
+                 void* v_pages, const pa_dims_t* dims, hipStream_t stream) {
+  if (dims == nullptr) return PA_EINVAL;
+  const pa_dims_t* d = dims;
+  if (d->num_seqs < 0 || d->num_kv_heads <= 0 || d->num_pages < 0 || d->max_pages_per_seq < 0 ||
+      d->max_context_len < 0)
+    return PA_EINVAL;
+  if (d->dtype != PA_BF16 && d->dtype != PA_FP32) return PA_ENOTSUP;
+  if (d->head_dim != 64 && d->head_dim != 128) return PA_ENOTSUP;
+  if (d->page_size != 16) return PA_ENOTSUP;
+  if (((int64_t)d->max_context_len + 15) / 16 > d->max_pages_per_seq) return PA_EINVAL;
+  int rows;
+  if (query_start_loc != nullptr) {
+    if (d->num_q_rows < 0) return PA_EINVAL;
+    if (d->num_q_rows > 0 && d->num_seqs == 0) return PA_EINVAL;
+    rows = d->num_q_rows;
+  } else {
+    if (d->num_q_rows != 0 && d->num_q_rows != d->num_seqs) return PA_EINVAL;
+    rows = d->num_seqs;
+  }
+  if (rows == 0) return PA_OK;
+  if (!k_new || !v_new || !block_table || !context_lens || !k_pages || !v_pages) return PA_EINVAL;
+  pa::AppendArgs a;
+  a.k_new = static_cast<const uint8_t*>(k_new);
+  a.v_new = static_cast<const uint8_t*>(v_new);
+  a.k_pages = static_cast<uint8_t*>(k_pages);
+  a.v_pages = static_cast<uint8_t*>(v_pages);
+  a.block_table = block_table;
+  a.context_lens = context_lens;
+  a.query_start_loc = query_start_loc;
+  a.bt_stride = d->max_pages_per_seq;
+  a.B = d->num_seqs;
+  a.rows = rows;
+  a.H_kv = d->num_kv_heads;
+  a.row_bytes = d->head_dim * (d->dtype == PA_BF16 ? 2 : 4);
+  a.num_pages = d->num_pages;
+  a.max_context_len = d->max_context_len;
+  return pa::launch_kv_append(a, stream) == hipSuccess ? PA_OK : PA_EHIP;
+}
+
 const char* pa_strerror(int code) {
   switch (code) {
     case PA_OK: return "success";

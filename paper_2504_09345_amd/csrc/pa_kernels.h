@@ -104,6 +104,22 @@ bool prefill_supported(int dtype, int D, int s);
 int prefill_occupancy(int s, int B);  // workgroups per CU, 0 on error
 hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st);
 
+// Arguments of the KV-append (cache write) kernel.  query_start_loc == nullptr
+// is the decode layout (row b appends position context_lens[b] - 1).
+struct AppendArgs {
+  const uint8_t* k_new;
+  const uint8_t* v_new;
+  uint8_t* k_pages;
+  uint8_t* v_pages;
+  const int32_t* block_table;
+  const int32_t* context_lens;
+  const int32_t* query_start_loc;
+  int64_t bt_stride;
+  int B, rows, H_kv, row_bytes, num_pages, max_context_len;
+};
+
+hipError_t launch_kv_append(const AppendArgs& a, hipStream_t st);
+
 // dtype: 0 bf16, 1 fp32.  Return hipSuccess or the launch error.
 hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st);
 hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st);

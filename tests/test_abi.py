@@ -223,3 +223,50 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(pb, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="no fallback"):
         pb.load()
+
+
+@host_only
+@pytest.mark.parametrize("case", ["null_dims", "null_knew", "null_pool", "fp16", "hd", "page",
+                                  "table_short", "decode_rows", "neg_rows", "rows_no_seqs"])
+def test_kv_append_validation(case):
+    import ctypes
+    d = dims()
+    args = dict(kn=FAKE, vn=FAKE, bt=FAKE, cl=FAKE, qsl=None, kp=FAKE, vp=FAKE)
+    expect = pb.PA_EINVAL
+    if case == "null_knew":
+        args["kn"] = None
+    elif case == "null_pool":
+        args["vp"] = None
+    elif case == "fp16":
+        d.dtype = 7
+        expect = pb.PA_ENOTSUP
+    elif case == "hd":
+        d.head_dim = 96
+        expect = pb.PA_ENOTSUP
+    elif case == "page":
+        d.page_size = 32
+        expect = pb.PA_ENOTSUP
+    elif case == "table_short":
+        d.max_pages_per_seq = 100
+    elif case == "decode_rows":
+        d.num_q_rows = 7
+    elif case == "neg_rows":
+        args["qsl"] = FAKE
+        d.num_q_rows = -1
+    elif case == "rows_no_seqs":
+        args["qsl"] = FAKE
+        d.num_seqs, d.num_q_rows = 0, 5
+    lib = pb.load()
+    rc = lib.pa_kv_append(args["kn"], args["vn"], args["bt"], args["cl"], args["qsl"], args["kp"],
+                          args["vp"], None if case == "null_dims" else ctypes.byref(d), None)
+    assert rc == expect
+
+
+@host_only
+def test_kv_append_without_rows_touches_nothing():
+    import ctypes
+    lib = pb.load()
+    d = dims(num_seqs=0)
+    assert lib.pa_kv_append(None, None, None, None, None, None, None, ctypes.byref(d), None) == pb.PA_OK
+    d = dims(num_q_rows=0)
+    assert lib.pa_kv_append(None, None, None, None, FAKE, None, None, ctypes.byref(d), None) == pb.PA_OK
