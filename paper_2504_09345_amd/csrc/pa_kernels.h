@@ -101,6 +101,11 @@ struct PrefillArgs {
 };
 
 bool prefill_supported(int dtype, int D, int s);
+
+// Mixed batch in one launch: G_dec stream-K decode workgroups and G - G_dec
+// prefill workgroups (bf16, head_dim 128, W = 8 decode waves).
+bool mixed_supported(int dtype, int D, int s, int W);
+hipError_t launch_mixed(int s, const StreamArgs& sa, const PrefillArgs& pa, int G_dec, int G, hipStream_t st);
 int prefill_occupancy(int s, int B);  // workgroups per CU, 0 on error
 hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st);
 

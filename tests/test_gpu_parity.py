@@ -236,7 +236,7 @@ def test_stream_handles_more_workgroups_than_pages():
 
 # --- MFMA chunked prefill ---------------------------------------------------
 
-def _chunk_batch(s, seed, chunks, decode_ctx, dtype="bf16", poison=False):
+def _chunk_batch(s, seed, chunks, decode_ctx, dtype="bf16", poison=False, H_kv=2):
     """Sequences with (chunk length L, prior cached tokens) plus decode rows,
     interleaved, identity-free random page placement."""
     rng = np.random.default_rng(seed)
@@ -246,10 +246,10 @@ def _chunk_batch(s, seed, chunks, decode_ctx, dtype="bf16", poison=False):
     ctx = [L + prior for L, prior in seqs]
     qlen = [L for L, _ in seqs]
     b = W.generate("tiny", seed=seed, dtype=dtype, poison=poison,
-                   overrides=dict(H_q=2 * s, H_kv=2, D=128, ctx=("list", ctx), pool=("factor", 1.4)))
+                   overrides=dict(H_q=H_kv * s, H_kv=H_kv, D=128, ctx=("list", ctx), pool=("factor", 1.4)))
     # re-draw q with one row per query position
     T = int(sum(qlen))
-    q = W._fill_normal((T, 2 * s, 128), seed + 1, "q", 1.0, dtype, 1)
+    q = W._fill_normal((T, H_kv * s, 128), seed + 1, "q", 1.0, dtype, 1)
     qsl = np.zeros(len(seqs) + 1, np.int32)
     qsl[1:] = np.cumsum(qlen)
     return W.Batch(**{**b.__dict__, "q": q, "query_start_loc": qsl})
@@ -263,6 +263,18 @@ def test_prefill_chunks_mfma(s):
     got = run_gpu(b)
     ref = run_oracle(b)
     assert_parity(got, ref, strict=False, what=f"prefill s={s}")
+
+
+@pytest.mark.parametrize("s", [1, 2, 4, 6, 8])
+def test_mixed_batch_one_launch(s):
+    """8 KV heads: decode rows and prefill chunks run as the two halves of one
+    mixed launch (decode workgroups and prefill workgroups side by side)."""
+    announce(f"mixed one launch s={s}")
+    chunks = [(17, 5), (100, 0), (64, 600), (130, 300), (2, 40)]
+    b = _chunk_batch(s, 60 + s, chunks, decode_ctx=[1, 16, 300, 2000, 777, 64], H_kv=8)
+    got = run_gpu(b)
+    assert_parity(got, run_oracle(b), strict=False, what=f"mixed s={s}")
+    assert np.array_equal(got.view(np.uint32), run_gpu(b).view(np.uint32))
 
 
 def test_prefill_poisoned_pool():
