@@ -99,10 +99,12 @@ typedef struct pa_dims {
 } pa_dims_t;
 
 /* Optional timing hooks: when a pa_timing_t* is passed and an event is
- * non-NULL, it is recorded on the call's stream at that point: attn_begin
- * before the first attention kernel, attn_end right after the attention
- * kernel(s), reduce_end after the kernel that merges split partial results
- * (recorded even when none was needed). */
+ * non-NULL, it is recorded for the call: attn_begin when the first attention
+ * kernel starts executing and attn_end when the last attention kernel ends
+ * (both taken by the kernel launches themselves, so their difference is the
+ * kernels' own duration), and reduce_end on the call's stream after the
+ * kernel that merges split partial results (recorded even when none was
+ * needed). */
 typedef struct pa_timing {
   hipEvent_t attn_begin;
   hipEvent_t attn_end;

@@ -138,7 +138,6 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
   }
 
   char* ws = static_cast<char*>(workspace);
-  record(ev_begin, stream);
   hipError_t e = hipSuccess;
   pa::StreamArgs sa{};
   int G = 0;
@@ -179,8 +178,20 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
   // mixed batch: decode and prefill workgroups side by side in one launch
   const bool mixed = p.stream && p.prefill && dims->num_seqs > 0 &&
                      pa::mixed_supported(dims->dtype, dims->head_dim, p.s, p.W);
+  // attention kernels in launch order: stream-K (or mixed), prefill, split-K;
+  // the timing events bracket the first one's start and the last one's end
+  // (rows > 0 here, so every planned kernel launches)
+  const int n_attn = (p.stream ? 1 : 0) + (p.prefill && !mixed ? 1 : 0) + (p.split ? 1 : 0);
+  int n_launched = 0;
+  auto next_events = [&]() {
+    pa::KernelEvents k;
+    k.start = n_launched == 0 ? ev_begin : nullptr;
+    k.stop = n_launched == n_attn - 1 ? ev_attn : nullptr;
+    ++n_launched;
+    return k;
+  };
   if (p.stream && !mixed && sa.B > 0) {
-    e = pa::launch_stream(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream);
+    e = pa::launch_stream(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream, next_events());
     if (e != hipSuccess) return PA_EHIP;
   }
   if (p.prefill) {
@@ -207,11 +218,11 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
       // (measured on the mixed Mixtral batch: splits 176..208 / 48..80 of the
       // 256 CUs are within 2 % of this one)
       const int g_pf = cus - G > cus / 4 ? cus - G : (cus / 4 > 0 ? cus / 4 : 1);
-      e = pa::launch_mixed(p.s, sa, pf, G, G + g_pf, stream);
+      e = pa::launch_mixed(p.s, sa, pf, G, G + g_pf, stream, next_events());
     } else {
       const int per_cu = pa::prefill_occupancy(p.s, dims->num_seqs);
       if (per_cu <= 0) return PA_EHIP;
-      e = pa::launch_prefill(p.s, pf, per_cu * cus, stream);
+      e = pa::launch_prefill(p.s, pf, per_cu * cus, stream, next_events());
     }
     if (e != hipSuccess) return PA_EHIP;
   }
@@ -236,10 +247,13 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     a.pages_per_split = p.pps;
     a.n_split_slots = p.n_split_slots;
     a.skip_single_rows = p.stream ? 1 : 0;
-    e = pa::launch_decode(dims->dtype, dims->head_dim, p.s, a, p.rows, stream);
+    e = pa::launch_decode(dims->dtype, dims->head_dim, p.s, a, p.rows, stream, next_events());
     if (e != hipSuccess) return PA_EHIP;
   }
-  record(ev_attn, stream);
+  if (n_launched == 0) {  // (cannot happen with rows > 0; keeps the events consistent)
+    record(ev_begin, stream);
+    record(ev_attn, stream);
+  }
   if (p.stream && sa.B > 0) {
     e = pa::launch_stream_fixup(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream);
     if (e != hipSuccess) return PA_EHIP;

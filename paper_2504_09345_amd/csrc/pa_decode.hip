@@ -216,28 +216,32 @@ __global__ __launch_bounds__(256) void gather_trace_kernel(BlockTable bt, const 
 // ---- launchers -----------------------------------------------------------
 
 template <typename T, int D>
-static hipError_t decode_s(int s, const DecodeArgs& a, int rows, hipStream_t st) {
+static const void* decode_fn(int s) {
+  switch (s) {
+    case 1: return reinterpret_cast<const void*>(&decode_kernel<T, D, 1, kDecodeWaves, kDecodeRing>);
+    case 2: return reinterpret_cast<const void*>(&decode_kernel<T, D, 2, kDecodeWaves, kDecodeRing>);
+    case 4: return reinterpret_cast<const void*>(&decode_kernel<T, D, 4, kDecodeWaves, kDecodeRing>);
+    case 6: return reinterpret_cast<const void*>(&decode_kernel<T, D, 6, kDecodeWaves, kDecodeRing>);
+    case 8: return reinterpret_cast<const void*>(&decode_kernel<T, D, 8, kDecodeWaves, kDecodeRing>);
+  }
+  return nullptr;
+}
+
+hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st, KernelEvents ev) {
+  const void* fn = nullptr;
+  if (dtype == 0 && D == 128) fn = decode_fn<uint16_t, 128>(s);
+  else if (dtype == 0 && D == 64) fn = decode_fn<uint16_t, 64>(s);
+  else if (dtype == 1 && D == 128) fn = decode_fn<float, 128>(s);
+  else if (dtype == 1 && D == 64) fn = decode_fn<float, 64>(s);
+  if (fn == nullptr) return hipErrorInvalidValue;
   const int64_t n = (int64_t)rows * a.H_kv * a.n_split_slots;
   if (n == 0) return hipSuccess;
   if (n > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-  const dim3 grid((unsigned)n), block(64 * kDecodeWaves);
-  switch (s) {
-    case 1: decode_kernel<T, D, 1, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
-    case 2: decode_kernel<T, D, 2, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
-    case 4: decode_kernel<T, D, 4, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
-    case 6: decode_kernel<T, D, 6, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
-    case 8: decode_kernel<T, D, 8, kDecodeWaves, kDecodeRing><<<grid, block, 0, st>>>(a); break;
-    default: return hipErrorInvalidValue;
-  }
+  DecodeArgs a0 = a;
+  void* args[] = {&a0};
+  hipError_t e = hipExtLaunchKernel(fn, dim3((unsigned)n), dim3(64 * kDecodeWaves), args, 0, st, ev.start, ev.stop, 0);
+  if (e != hipSuccess) return e;
   return hipGetLastError();
-}
-
-hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st) {
-  if (dtype == 0 && D == 128) return decode_s<uint16_t, 128>(s, a, rows, st);
-  if (dtype == 0 && D == 64) return decode_s<uint16_t, 64>(s, a, rows, st);
-  if (dtype == 1 && D == 128) return decode_s<float, 128>(s, a, rows, st);
-  if (dtype == 1 && D == 64) return decode_s<float, 64>(s, a, rows, st);
-  return hipErrorInvalidValue;
 }
 
 hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st) {

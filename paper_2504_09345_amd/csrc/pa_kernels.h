@@ -1,6 +1,8 @@
 // Host-side launchers of the gfx950 kernels (internal to libpagedattn.so).
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -81,7 +83,15 @@ constexpr int kStreamMaxWaves = PA_STREAM_MAX_WAVES;  // waves (KV heads) per st
 #endif
 constexpr bool kStreamMfma = PA_STREAM_MFMA != 0;  // bf16 D = 128 tiles on the matrix cores
 
-hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
+// Optional events bracketing one kernel's execution (hipExtLaunchKernel's
+// start/stop events: taken when the kernel starts and ends, not when the
+// stream reaches the launch).  Null members record nothing.
+struct KernelEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
+hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st,
+                         KernelEvents ev = {});
 hipError_t launch_stream_fixup(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
 int stream_occupancy(int dtype, int D, int s, int W);  // workgroups per CU, 0 on error
 
@@ -105,9 +115,10 @@ bool prefill_supported(int dtype, int D, int s);
 // Mixed batch in one launch: G_dec stream-K decode workgroups and G - G_dec
 // prefill workgroups (bf16, head_dim 128, W = 8 decode waves).
 bool mixed_supported(int dtype, int D, int s, int W);
-hipError_t launch_mixed(int s, const StreamArgs& sa, const PrefillArgs& pa, int G_dec, int G, hipStream_t st);
+hipError_t launch_mixed(int s, const StreamArgs& sa, const PrefillArgs& pa, int G_dec, int G, hipStream_t st,
+                        KernelEvents ev = {});
 int prefill_occupancy(int s, int B);  // workgroups per CU, 0 on error
-hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st);
+hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st, KernelEvents ev = {});
 
 // Arguments of the KV-append (cache write) kernel.  query_start_loc == nullptr
 // is the decode layout (row b appends position context_lens[b] - 1).
@@ -126,7 +137,8 @@ struct AppendArgs {
 hipError_t launch_kv_append(const AppendArgs& a, hipStream_t st);
 
 // dtype: 0 bf16, 1 fp32.  Return hipSuccess or the launch error.
-hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st);
+hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st,
+                         KernelEvents ev = {});
 hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st);
 hipError_t launch_gather_trace(const int32_t* block_table, int64_t bt_stride,
                                const int32_t* context_lens, const int64_t* row_start, int B,

@@ -55,14 +55,15 @@ bool mixed_supported(int dtype, int D, int s, int W) {
   return kStreamMfma && dtype == 0 && D == mfma::kD && W == kMixedW && mixed_fn(s) != nullptr;
 }
 
-hipError_t launch_mixed(int s, const StreamArgs& sa, const PrefillArgs& pa_, int G_dec, int G, hipStream_t st) {
+hipError_t launch_mixed(int s, const StreamArgs& sa, const PrefillArgs& pa_, int G_dec, int G, hipStream_t st,
+                        KernelEvents ev) {
   const void* fn = mixed_fn(s);
   if (fn == nullptr || G_dec <= 0 || G <= G_dec) return hipErrorInvalidValue;
   StreamArgs a0 = sa;
   PrefillArgs a1 = pa_;
   int g = G_dec;
   void* args[] = {&a0, &a1, &g};
-  hipError_t e = hipLaunchKernel(fn, dim3(G), dim3(64 * kMixedW), args, 0, st);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(G), dim3(64 * kMixedW), args, 0, st, ev.start, ev.stop, 0);
   if (e != hipSuccess) return e;
   return hipGetLastError();
 }

@@ -65,11 +65,12 @@ int prefill_occupancy(int s, int B) {
   return n;
 }
 
-hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st) {
+hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st, KernelEvents ev) {
   const void* fn = prefill_fn(s);
   if (fn == nullptr || G <= 0) return hipErrorInvalidValue;
   void* args[] = {const_cast<PrefillArgs*>(&a)};
-  hipError_t e = hipLaunchKernel(fn, dim3(G), dim3(kPfThreads), args, (size_t)(a.B + 1) * sizeof(int32_t), st);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(G), dim3(kPfThreads), args, (size_t)(a.B + 1) * sizeof(int32_t), st,
+                                    ev.start, ev.stop, 0);
   if (e != hipSuccess) return e;
   return hipGetLastError();
 }

@@ -165,11 +165,12 @@ static bool fixup_s(int s, int W, const StreamArgs& a, int G, hipStream_t st) {
   return false;
 }
 
-hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st) {
+hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st,
+                         KernelEvents ev) {
   const void* fn = stream_kernel_fn(dtype, D, s, W);
   if (fn == nullptr || G <= 0) return hipErrorInvalidValue;
   void* args[] = {const_cast<StreamArgs*>(&a)};
-  hipError_t e = hipLaunchKernel(fn, dim3(G), dim3(64 * W), args, 0, st);
+  hipError_t e = hipExtLaunchKernel(fn, dim3(G), dim3(64 * W), args, 0, st, ev.start, ev.stop, 0);
   if (e != hipSuccess) return e;
   return hipGetLastError();
 }
