@@ -1,10 +1,10 @@
 #!/usr/bin/env python3
 """Benchmark of the paged GQA decode-attention hot path on one MI355X.
 
-One step = one paged_attn call (stream-K attention kernel + the fixup that
-merges split items; for the mixed workload one paged_attn_varlen call, which
-adds the chunked-prefill kernel) over a whole synthetic batch whose inputs
-are already resident in HBM.
+One step = one paged_attn call (the stream-K attention kernel, which also
+merges the items its ranges cut; for the mixed workload one paged_attn_varlen
+call, whose one kernel runs the decode rows and the prefill chunks side by
+side) over a whole synthetic batch whose inputs are already resident in HBM.
 Default workload: Mixtral-8x7B-shaped decode, batch 256, 32 query / 8 KV
 heads, head dim 128, bf16 KV, page size 16, context lengths uniform in
 [512, 2048], pages randomly placed in a pool 1.25x the need.
@@ -18,8 +18,8 @@ synchronisation (the throughput figure).  The K/V pools are replicated R
 times and the steps rotate through the copies, so each step streams its KV
 from HBM and not from the 256 MB last-level cache left warm by the previous
 step.  A second pass of K steps, outside the timed region, has the library
-record HIP events on the launch stream around the attention kernel(s) and the
-fixup; their durations give the roofline figures.
+record HIP events bracketing the attention kernel(s); their durations give the
+roofline figures.
 """
 from __future__ import annotations
 

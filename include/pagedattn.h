@@ -25,9 +25,11 @@
  *
  * Conventions for every entry point
  *   - All array pointers are DEVICE pointers (HBM), except where a name ends
- *     in _host.  The caller owns every buffer; the library allocates nothing
- *     and keeps no state between calls, so calls on different streams may
- *     overlap as long as their output and workspace buffers do not.
+ *     in _host.  The caller owns every buffer; the library allocates nothing.
+ *     Its only state between calls is a process-wide counter that tags each
+ *     call's use of the workspace (it never changes a result).  Calls on
+ *     different streams may overlap as long as their output and workspace
+ *     buffers do not.
  *   - Work is enqueued on `stream` (NULL = the null stream) and the call
  *     returns without synchronising.  Faults inside kernels (for example a
  *     block-table entry outside the pool) surface at the caller's next
@@ -113,7 +115,7 @@ typedef struct pa_timing {
 
 /* Bytes of device workspace a paged_attn / paged_attn_varlen call with these
  * dims needs: partial outputs and softmax statistics of items split across
- * workgroups, and per-sequence page prefix sums.  Writes 0 when no workspace
+ * workgroups, and per-workgroup flags that publish them.  Writes 0 when no workspace
  * is needed.  A call whose dims carry chunked rows (max_q_len > 1 or
  * num_q_rows != num_seqs) is sized as varlen.  Host only; no HIP call.
  * Errors: PA_EINVAL / PA_ENOTSUP as for paged_attn. */
@@ -121,10 +123,10 @@ int pa_workspace_size(const pa_dims_t *dims, size_t *bytes);
 
 /* Decode attention: one query row per sequence (Sec. 6.6 computes exactly
  * this on the CPU).  Here: a persistent stream-K kernel over equal ranges of
- * (sequence, KV-head block, page) units plus a fixup kernel that merges the
- * items cut by range boundaries; with pages_per_split > 0, or more than 8192
- * sequences, a per-row split-K kernel plus a reduction kernel.  Both are
- * deterministic (no float atomics).
+ * (sequence, KV-head block, page) units whose workgroups also merge the
+ * items cut by range boundaries (one launch); with pages_per_split > 0, or
+ * more than 8192 sequences, a per-row split-K kernel plus a reduction kernel.
+ * Both are deterministic (no float atomics; merges run in a fixed order).
  *   q            [num_seqs][H_q][D]        device, read
  *   k_pages,
  *   v_pages      pool, see layouts above   device, read

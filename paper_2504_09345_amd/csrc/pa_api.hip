@@ -1,10 +1,13 @@
 // C ABI of libpagedattn.so: host-side validation, launch planning and
 // dispatch.  Validation runs before any HIP call, so a rejected call enqueues
-// nothing and is testable without a GPU.  The library allocates nothing and
-// keeps no state between calls.
+// nothing and is testable without a GPU.  The library allocates nothing; its
+// only state between calls is the counter that tags each call's range flags.
 #include <math.h>
 #include <stddef.h>
 #include <stdint.h>
+
+#include <atomic>
+#include <chrono>
 
 #include "pa_kernels.h"
 #include "pagedattn.h"
@@ -83,7 +86,7 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
     const size_t recs = (size_t)pa::kStreamMaxGrid * 2 * p->W * s;  // (workgroup, slot, wave, head)
     p->st_o = align256(recs * (size_t)d->head_dim * sizeof(float));
     p->st_ml = align256(recs * 2 * sizeof(float));
-    p->st_cum = align256(((size_t)d->num_seqs + 1) * sizeof(int32_t));
+    p->st_cum = align256((size_t)pa::kStreamMaxGrid * sizeof(unsigned long long));  // range flags
   }
   // chunked-prefill rows of a varlen call: MFMA kernel (bf16, head_dim 128)
   p->prefill = varlen && p->stream && pa::prefill_supported(d->dtype, d->head_dim, s);
@@ -106,6 +109,18 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
   }
   p->ws_bytes = p->st_o + p->st_ml + p->st_cum + p->sp_o + p->sp_ml;
   return PA_OK;
+}
+
+// Tag of one call's range flags in the workspace: process-wide, never 0 and
+// never repeated, so flags left in a reused workspace by earlier calls (or
+// found in a fresh one) do not match.  This counter is the library's only
+// state; it does not influence any result.
+unsigned long long next_token() {
+  static std::atomic<unsigned long long> counter{
+      0x9e3779b97f4a7c15ull ^
+      (unsigned long long)std::chrono::steady_clock::now().time_since_epoch().count()};
+  unsigned long long t = counter.fetch_add(1, std::memory_order_relaxed) + 1;
+  return t != 0 ? t : counter.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
 void record(hipEvent_t ev, hipStream_t st) {
@@ -166,7 +181,8 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     sa.out = out;
     sa.ws_o = reinterpret_cast<float*>(ws);
     sa.ws_ml = reinterpret_cast<float*>(ws + p.st_o);
-    sa.ws_cum = reinterpret_cast<int32_t*>(ws + p.st_o + p.st_ml);
+    sa.ws_flag = reinterpret_cast<unsigned long long*>(ws + p.st_o + p.st_ml);
+    sa.token = next_token();
     sa.bt_stride = dims->max_pages_per_seq;
     sa.scale_log2 = scale * 1.4426950408889634f;
     sa.B = dims->num_seqs;
@@ -253,10 +269,6 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
   if (n_launched == 0) {  // (cannot happen with rows > 0; keeps the events consistent)
     record(ev_begin, stream);
     record(ev_attn, stream);
-  }
-  if (p.stream && sa.B > 0) {
-    e = pa::launch_stream_fixup(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream);
-    if (e != hipSuccess) return PA_EHIP;
   }
   if (p.split && p.n_split_slots > 1) {
     pa::ReduceArgs r{};

@@ -83,6 +83,26 @@ template <int OFF> __device__ __forceinline__ float xor_lanes(float v) {
   else return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x1F | (OFF << 10)));
 }
 
+// Partial records of the stream-K kernel are exchanged between workgroups of
+// one launch that may sit on different XCDs, whose L2 caches are not coherent
+// with each other.  They are written and read with device-scope relaxed
+// atomics (coherent at the device level, no L2 writeback or invalidate of the
+// whole cache), 8 bytes at a time.
+__device__ __forceinline__ void store_dev(float* p, float a, float b) {
+  const unsigned long long v = (unsigned long long)__float_as_uint(a) | (unsigned long long)__float_as_uint(b) << 32;
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void load_dev2(const float* p, float& a, float& b) {
+  const unsigned long long v =
+      __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  a = __uint_as_float((uint32_t)v);
+  b = __uint_as_float((uint32_t)(v >> 32));
+}
+__device__ __forceinline__ float load_dev(const float* p) {
+  return __uint_as_float(__hip_atomic_load(reinterpret_cast<const unsigned int*>(p), __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT));
+}
+
 // Lazy rebasing of the online softmax (matrix-core paths): a row's running
 // max m is moved only when a new score exceeds it by more than this many log2
 // units; until then weights exp2(x - m) stay below 2^kRescaleSlack and the

@@ -47,7 +47,7 @@ struct ReduceArgs {
   int skip_single_rows;
 };
 
-// Arguments of the persistent stream-K kernel and its fixup.  Items are
+// Arguments of the persistent stream-K kernel.  Items are
 // (sequence, KV head); for varlen calls only sequences with exactly one
 // query row are taken (chunked prefill rows go to the per-row kernel).
 struct StreamArgs {
@@ -60,7 +60,8 @@ struct StreamArgs {
   void* out;
   float* ws_o;       // [G][2][W][s][D] partial outputs (slot 0 head, 1 tail)
   float* ws_ml;      // [G][2][W][s][2]
-  int32_t* ws_cum;   // [B+1] page prefix sums, written by workgroup 0
+  unsigned long long* ws_flag;  // [G] set to `token` once a range's head record is written
+  unsigned long long token;     // tag of this call (never 0; differs from every earlier call's)
   int64_t bt_stride;
   float scale_log2;
   int B, H_q, H_kv, max_context_len;
@@ -92,7 +93,6 @@ struct KernelEvents {
 
 hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st,
                          KernelEvents ev = {});
-hipError_t launch_stream_fixup(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st);
 int stream_occupancy(int dtype, int D, int s, int W);  // workgroups per CU, 0 on error
 
 // Arguments of the MFMA chunked-prefill kernel (bf16, head_dim 128): the rows

@@ -6,10 +6,11 @@
 // prefill is matrix-core bound.  Giving the decode rows G_dec workgroups and
 // the prefill chunks the remaining CUs runs the two side by side instead of
 // one after the other.  Workgroups [0, G_dec) run the stream-K body over the
-// decode units exactly as the stream kernel would with a grid of G_dec (its
-// partial records and fixup are unchanged); workgroups [G_dec, grid) run the
-// prefill body with a grid of grid - G_dec.  No workgroup waits on another,
-// so the split is correct whatever the residency.  The two bodies' LDS
+// decode units exactly as the stream kernel would with a grid of G_dec
+// (including the merge of cut items); workgroups [G_dec, grid) run the
+// prefill body with a grid of grid - G_dec.  No prefill workgroup waits on
+// another, and decode workgroups only wait on higher decode ranges, so the
+// split is correct whatever the residency.  The two bodies' LDS
 // layouts share one union.
 #include "pa_prefill_body.h"
 #include "pa_stream_body.h"

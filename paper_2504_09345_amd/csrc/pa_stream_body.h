@@ -17,6 +17,60 @@ __device__ __forceinline__ bool info_end(int i) { return (i >> 6) & 1; }
 __device__ __forceinline__ int info_hb(int i) { return (i >> 7) & 63; }
 __device__ __forceinline__ int info_row(int i) { return (int)((unsigned)i >> 13); }
 
+// Merge the partial records of item (row r, KV head g) held by ranges
+// wg_first .. wg_last (record slot 1 of wg_first, slot 0 of the others; empty
+// ranges wrote nothing) and write the output row: one wave, E elements per
+// lane, records merged in range order.
+template <typename T, int D, int S, int W>
+__device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64_t G, int64_t wg_first,
+                                           int64_t wg_last, int w, int lane, T* out) {
+  constexpr int E = S * D / 64;  // elements per lane
+  float M[S], L[S], acc[E];
+#pragma unroll
+  for (int j = 0; j < S; ++j) { M[j] = kMInit; L[j] = 0.0f; }
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+  // pass 1: maxima
+  for (int64_t x = wg_first; x <= wg_last; ++x) {
+    if (U * x / G == U * (x + 1) / G) continue;  // empty range wrote nothing
+    const int64_t slot = (x * 2 + (x == wg_first ? 1 : 0)) * W + w;
+#pragma unroll
+    for (int j = 0; j < S; ++j) M[j] = fmaxf(M[j], load_dev(a.ws_ml + slot * S * 2 + j * 2));
+  }
+  // pass 2: weighted sums
+  for (int64_t x = wg_first; x <= wg_last; ++x) {
+    if (U * x / G == U * (x + 1) / G) continue;
+    const int64_t slot = (x * 2 + (x == wg_first ? 1 : 0)) * W + w;
+    float c[S];
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      c[j] = fast_exp2(load_dev(a.ws_ml + slot * S * 2 + j * 2) - M[j]);
+      L[j] = fmaf(load_dev(a.ws_ml + slot * S * 2 + j * 2 + 1), c[j], L[j]);
+    }
+    const float* o = a.ws_o + slot * S * D;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int idx = lane * E + e;
+      acc[e] = fmaf(load_dev(o + idx), c[idx / D], acc[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int idx = lane * E + e;
+    store_out<T>(out + idx, acc[e] / L[idx / D]);
+  }
+}
+
+// Sequence of unit u: the largest r with nb * cum[r] <= u (a non-empty one).
+__device__ __forceinline__ int info_row_seq(const int32_t* cum, int R, int nb, int64_t u) {
+  int lo = 0, hi = R - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((int64_t)nb * cum[mid] <= u) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
 // LDS of one stream-K workgroup.
 template <int W, bool MF>
 struct StreamSmem {
@@ -51,7 +105,7 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
       int row, nv;
       int np = seq_decode_row(a.query_start_loc, a.context_lens, a.max_context_len, r, row, nv) == 1
                    ? (nv + kPage - 1) / kPage : 0;
-      if (np > (int)a.bt_stride) np = 0;  // contract violation: the fixup writes NaN
+      if (np > (int)a.bt_stride) np = 0;  // contract violation: a NaN row (below)
       s_tail[r] = (uint8_t)(np ? nv - (np - 1) * kPage : 0);
       s_cum[r] = local;
       local += np;
@@ -62,9 +116,18 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
     __syncthreads();
   }
   const int64_t U = (int64_t)a.nb * s_cum[R];
-  if (bid == 0)
-    for (int r = tid; r <= R; r += NT) a.ws_cum[r] = s_cum[r];
   const int64_t G = G_;
+  // Rows without units: zeros for an empty decode context, NaN for a contract
+  // violation; rows r = bid (mod G) are this workgroup's to write.
+  for (int r = bid; r < R; r += G_) {
+    int qrow, nv;
+    const int status = seq_decode_row(a.query_start_loc, a.context_lens, a.max_context_len, r, qrow, nv);
+    const int np = status == 1 ? (nv + kPage - 1) / kPage : 0;
+    if (status == 0 || (status == 1 && np > 0 && np <= (int)a.bt_stride)) continue;
+    const float fill = (status < 0 || np > (int)a.bt_stride) ? NAN : 0.0f;
+    T* o = reinterpret_cast<T*>(a.out) + (int64_t)qrow * a.H_q * D;
+    for (int i = tid; i < a.H_q * D; i += NT) store_out<T>(o + i, fill);
+  }
   const int64_t u0 = U * bid / G, u1 = U * (bid + 1) / G;
   const int n_units = (int)(u1 - u0);
   if (n_units <= 0) return;
@@ -73,12 +136,7 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
   const BlockTable bt{a.block_table, a.bt_stride};
   for (int i = tid; i < n_units; i += NT) {
     const int64_t u = u0 + i;
-    int lo = 0, hi = R - 1;  // largest r with nb * cum[r] <= u (a non-empty sequence)
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if ((int64_t)a.nb * s_cum[mid] <= u) lo = mid; else hi = mid - 1;
-    }
-    const int r = lo;
+    const int r = info_row_seq(s_cum, R, a.nb, u);
     const int np = s_cum[r + 1] - s_cum[r];
     const int rem = (int)(u - (int64_t)a.nb * s_cum[r]);
     const int hb = rem / np, p = rem - hb * np;
@@ -118,6 +176,14 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
   u32x4 kr[NBUF][Sh::NI], vr[NBUF][Sh::NI];
 #pragma unroll
   for (int u = 0; u + 1 < NBUF; ++u) issue(kr[u], vr[u], u);
+  // A head record written at unit k is published one unit later, once the
+  // loads issued after it are the only ones outstanding: waiting for the
+  // record stores then does not drain the tile ring (the vector-memory
+  // counter retires loads and stores in issue order).
+  constexpr int kRingLoads = 2 * Sh::NI;  // load instructions of one issue()
+  constexpr int kWaitRing = (kRingLoads & 15) | (7 << 4) | (15 << 8) | ((kRingLoads >> 4) << 14);
+  static_assert(kRingLoads < 64, "vmcnt range");
+  bool publish = false;
   for (int base = 0; base < n_units; base += NBUF) {
 #pragma unroll
     for (int u = 0; u < NBUF; ++u) {
@@ -150,6 +216,12 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
         }
       }
       issue(kr[(u + NBUF - 1) % NBUF], vr[(u + NBUF - 1) % NBUF], k + NBUF - 1);
+      if (publish) {  // workgroup-uniform
+        publish = false;
+        __builtin_amdgcn_s_waitcnt(kWaitRing);  // everything but the tile just issued
+        __syncthreads();
+        if (tid == 0) __hip_atomic_store(a.ws_flag + bid, a.token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
       if (k < n_units) {
         if constexpr (MF)
           mfma::fold<S>(ms, kr[u], vr[u], s_kv[w], lane, info_valid(info), a.scale_log2);
@@ -164,13 +236,60 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
           if constexpr (MF) {
             if (!head_partial && !tail_partial)
               mfma::finish<S, T>(ms, lane, outp);
-            else
+            else if (head_partial)  // (the range holding the item's first part merges from registers)
               mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
           } else {
             if (!head_partial && !tail_partial)
               finish_rows<T, D, S>(st, row, dl, outp);
             else
               partial_rows<T, D, S>(st, row, dl, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
+          }
+          // Items cut by range boundaries (the branches are workgroup-uniform).
+          // Records travel through device-coherent stores and loads.  A range
+          // holding a later part publishes its head record: each wave waits
+          // for its record stores to complete, the barrier gathers the waves,
+          // then thread 0 sets the range's flag to this call's token (at the
+          // next unit, see above, unless the range ends here).  The
+          // range holding the item's first part waits for the later ranges'
+          // flags, then merges in range order: from its registers and the later
+          // records (matrix-core fold), or from every record (VALU fold, which
+          // stores its own tail record first).
+          // A range only ever waits on higher ranges, and writes its head
+          // record before it waits, so the waits always end.
+          if (head_partial) {
+            if (k + 1 < n_units) {
+              publish = true;  // at the next unit
+            } else {
+              __builtin_amdgcn_s_waitcnt(0);
+              __syncthreads();
+              if (tid == 0) __hip_atomic_store(a.ws_flag + bid, a.token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+          } else if (tail_partial) {
+            const int rr = info_row_seq(s_cum, R, a.nb, u0 + k);
+            const int np = s_cum[rr + 1] - s_cum[rr];
+            const int64_t e_last = (int64_t)a.nb * s_cum[rr] + (int64_t)info_hb(info) * np + np - 1;
+            const int64_t wg_last = ((e_last + 1) * G - 1) / U;
+            if constexpr (!MF) __builtin_amdgcn_s_waitcnt(0);  // this range's own tail record is stored
+            __syncthreads();
+            if (tid == 0) {
+              for (int64_t x = bid + 1; x <= wg_last; ++x) {
+                if (U * x / G == U * (x + 1) / G) continue;  // empty range: nothing to wait for
+                while (__hip_atomic_load(a.ws_flag + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.token)
+                  __builtin_amdgcn_s_sleep(4);
+              }
+            }
+            __syncthreads();
+            if constexpr (MF) {
+              // own part in registers, later ranges' head records folded in range order
+              for (int64_t x = bid + 1; x <= wg_last; ++x) {
+                if (U * x / G == U * (x + 1) / G) continue;
+                const int64_t sx = (x * 2) * W + w;
+                mfma::merge_record<S>(ms, a.ws_o + sx * S * D, a.ws_ml + sx * S * 2, lane);
+              }
+              mfma::finish<S, T>(ms, lane, outp);
+            } else {
+              merge_item<T, D, S, W>(a, U, G, bid, wg_last, w, lane, outp);
+            }
           }
         }
       }

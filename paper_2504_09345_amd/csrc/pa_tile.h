@@ -243,22 +243,12 @@ __device__ __forceinline__ void partial_rows(const DecodeState<T, D, S>& st, int
 #pragma unroll
     for (int j = 0; j < S; ++j) {
 #pragma unroll
-      for (int e = 0; e < Sh::VEC; e += 4) {
-        u32x4 w;
-        w.x = __float_as_uint(O[j][e]);
-        w.y = __float_as_uint(O[j][e + 1]);
-        w.z = __float_as_uint(O[j][e + 2]);
-        w.w = __float_as_uint(O[j][e + 3]);
-        *reinterpret_cast<u32x4*>(o + j * D + dl * Sh::VEC + e) = w;
-      }
+      for (int e = 0; e < Sh::VEC; e += 2) store_dev(o + j * D + dl * Sh::VEC + e, O[j][e], O[j][e + 1]);
     }
   }
   if (lane == 0) {
 #pragma unroll
-    for (int j = 0; j < S; ++j) {
-      ml[j * 2] = M[j];
-      ml[j * 2 + 1] = L[j];
-    }
+    for (int j = 0; j < S; ++j) store_dev(ml + j * 2, M[j], L[j]);
   }
 }
 
@@ -423,7 +413,39 @@ __device__ __forceinline__ void finish(const State<S>& st, int lane, T* out) {
   }
 }
 
-// Partial record: unnormalised O [s][D] and (M, L) per head.
+// Fold another range's partial record of the same item (unnormalised O
+// [s][D] and (M, L) per head, device-coherent loads) into the state: one
+// log-sum-exp merge step.  Afterwards the state's L is the item total so far.
+template <int S>
+__device__ __forceinline__ void merge_record(State<S>& st, const float* o, const float* ml, int lane) {
+  const int n = lane & 15, G = lane >> 4;
+  float L = total_l(st);
+  float mx = kMInit, lx = 0.0f;
+  f32x4_t ox[kD / 16];
+#pragma unroll
+  for (int mb = 0; mb < kD / 16; ++mb) ox[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if (n < S) {
+    load_dev2(ml + n * 2, mx, lx);
+#pragma unroll
+    for (int mb = 0; mb < kD / 16; ++mb) {
+      const int d = mb * 16 + 4 * G;
+      float x0, x1, x2, x3;
+      load_dev2(o + n * kD + d, x0, x1);
+      load_dev2(o + n * kD + d + 2, x2, x3);
+      ox[mb] = f32x4_t{x0, x1, x2, x3};
+    }
+  }
+  const float M = fmaxf(st.m, mx);
+  const float c0 = fast_exp2(st.m - M), c1 = fast_exp2(mx - M);
+#pragma unroll
+  for (int mb = 0; mb < kD / 16; ++mb) st.acc[mb] = st.acc[mb] * c0 + ox[mb] * c1;
+  L = fmaf(L, c0, lx * c1);
+  st.m = M;
+  st.l = L * 0.25f;  // the 4 lanes of a head each hold a quarter (exact)
+}
+
+// Partial record: unnormalised O [s][D] and (M, L) per head (device-coherent
+// stores: the record is read by another workgroup of the same launch).
 template <int S>
 __device__ __forceinline__ void partial(const State<S>& st, int lane, float* o, float* ml) {
   const float L = total_l(st);
@@ -432,12 +454,10 @@ __device__ __forceinline__ void partial(const State<S>& st, int lane, float* o, 
 #pragma unroll
     for (int mb = 0; mb < kD / 16; ++mb) {
       const int d = mb * 16 + 4 * G;
-      *reinterpret_cast<f32x4_t*>(o + n * kD + d) = st.acc[mb];
+      store_dev(o + n * kD + d, st.acc[mb][0], st.acc[mb][1]);
+      store_dev(o + n * kD + d + 2, st.acc[mb][2], st.acc[mb][3]);
     }
-    if (G == 0) {
-      ml[n * 2] = st.m;
-      ml[n * 2 + 1] = L;
-    }
+    if (G == 0) store_dev(ml + n * 2, st.m, L);
   }
 }
 

@@ -76,7 +76,7 @@ def _align(x):
 
 def _stream_ws(B, H_q, D):
     recs = 1024 * 2 * H_q  # (workgroup, slot) x (waves x group) = all query heads of a head block
-    return _align(recs * D * 4) + _align(recs * 2 * 4) + _align((B + 1) * 4)
+    return _align(recs * D * 4) + _align(recs * 2 * 4) + _align(1024 * 8)  # records, (m, l), range flags
 
 
 def _split_ws(rows, H_q, D, max_ctx, pps):
