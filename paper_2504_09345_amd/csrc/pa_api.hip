@@ -191,8 +191,16 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     sa.max_context_len = dims->max_context_len;
     sa.nb = p.nb;
   }
-  // mixed batch: decode and prefill workgroups side by side in one launch
+  // Mixed batch: decode and prefill workgroups side by side in one launch,
+  // unless the chunk rows outweigh the decode rows.  A decode row streams its
+  // whole KV (HBM-bound); a chunk row costs about s/80 of that on the matrix
+  // cores at equal context (Mixtral shapes: 4,096 chunk rows took 151 us on
+  // all CUs against 660 us for 512 decode rows).  Past half the decode work,
+  // a quarter of the CUs would hold the launch up; the kernels then run one
+  // after the other, prefill on every CU.
+  const int64_t chunk_rows = (int64_t)dims->num_q_rows - dims->num_seqs;
   const bool mixed = p.stream && p.prefill && dims->num_seqs > 0 &&
+                     chunk_rows * p.s <= (int64_t)40 * dims->num_seqs &&
                      pa::mixed_supported(dims->dtype, dims->head_dim, p.s, p.W);
   // attention kernels in launch order: stream-K (or mixed), prefill, split-K;
   // the timing events bracket the first one's start and the last one's end

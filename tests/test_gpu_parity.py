@@ -267,14 +267,27 @@ def test_prefill_chunks_mfma(s):
 
 @pytest.mark.parametrize("s", [1, 2, 4, 6, 8])
 def test_mixed_batch_one_launch(s):
-    """8 KV heads: decode rows and prefill chunks run as the two halves of one
-    mixed launch (decode workgroups and prefill workgroups side by side)."""
+    """8 KV heads and enough decode rows: decode rows and prefill chunks run as
+    the two halves of one mixed launch (decode and prefill workgroups side by
+    side; chunk rows x s <= 40 x sequences)."""
     announce(f"mixed one launch s={s}")
     chunks = [(17, 5), (100, 0), (64, 600), (130, 300), (2, 40)]
-    b = _chunk_batch(s, 60 + s, chunks, decode_ctx=[1, 16, 300, 2000, 777, 64], H_kv=8)
+    rng = np.random.default_rng(70 + s)
+    decode_ctx = [1, 16, 300, 2000, 777, 64] + rng.integers(1, 1500, 58).tolist()
+    assert (sum(L for L, _ in chunks) - len(chunks)) * s <= 40 * (len(chunks) + len(decode_ctx))
+    b = _chunk_batch(s, 60 + s, chunks, decode_ctx=decode_ctx, H_kv=8)
     got = run_gpu(b)
     assert_parity(got, run_oracle(b), strict=False, what=f"mixed s={s}")
     assert np.array_equal(got.view(np.uint32), run_gpu(b).view(np.uint32))
+
+
+def test_prefill_heavy_batch_runs_kernels_in_turn():
+    """Chunk rows outweigh the decode rows: stream-K then prefill on all CUs."""
+    announce("prefill-heavy batch")
+    chunks = [(300, 100), (250, 0), (400, 20)]
+    b = _chunk_batch(4, 80, chunks, decode_ctx=[5, 900], H_kv=8)
+    assert (sum(L for L, _ in chunks) - len(chunks)) * 4 > 40 * (len(chunks) + 2)
+    assert_parity(run_gpu(b), run_oracle(b), strict=False, what="prefill-heavy")
 
 
 def test_prefill_poisoned_pool():
