@@ -185,6 +185,9 @@ def main():
     ap.add_argument("--append", action="store_true",
                     help="each step first stores the step's new tokens' K/V into the cache "
                          "(pa_kv_append), then attends")
+    ap.add_argument("--overlap-gemm", action="store_true",
+                    help="also measure attention of one half of the batch overlapped with the "
+                         "other half's layer GEMMs on a second stream (adds an overlap_gemm object)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -348,11 +351,114 @@ def main():
     }
     if append is not None:
         res["kernels"]["kv_append"] = append
+    if args.overlap_gemm and args.workload in MODEL_GEMMS and qsl is None:
+        res["overlap_gemm"] = _overlap_gemm(torch, batch, dev_q, k0, v0, bt, cl, batch.scale,
+                                            max(5, min(K, 20)), args.workload)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = _cpu_baseline(batch, args.cpu_baseline_seconds, None)
         res["cpu_baseline"]["host_cpu"] = _cpu_model()
     print(json.dumps(res))
     return 0
+
+
+# Expert-FFN and projection shapes of the modelled MoE models (model dim h,
+# expert intermediate dim h_i, experts, top-k), for the synthetic GEMMs of the
+# attention / GEMM overlap measurement.
+MODEL_GEMMS = {
+    "mixtral-256": (4096, 14336, 8, 2),   # Mixtral-8x7B
+    "long-ctx-64": (4096, 14336, 8, 2),
+    "mixed": (4096, 14336, 8, 2),
+    "dbrx-512": (6144, 10752, 16, 4),     # DBRX
+}
+
+
+def _overlap_gemm(torch, batch, dev_q, k, v, bt, cl, scale, reps, workload):
+    """Two partitions of the decode batch, as in the paper's pipelined engine
+    (Sec. 6.4): attention of partition alpha (first half of the sequences) runs
+    on one stream while the layer GEMMs of partition beta (QKV and output
+    projections, top-k expert FFNs, random bf16 weights) run on another, on
+    the same GPU.  Reports each alone, both together, and whether attention's
+    output is bit-identical under the overlap."""
+    h, hi, E, topk = MODEL_GEMMS[workload]
+    B = batch.num_seqs
+    Ba, Bb = B // 2, B - B // 2
+    H_q, H_kv, D = batch.num_q_heads, batch.num_kv_heads, batch.head_dim
+    qa, bta, cla = dev_q[:Ba].contiguous(), bt[:Ba].contiguous(), cl[:Ba].contiguous()
+    mcl = int(batch.context_lens[:Ba].max())
+    dims = pb.make_dims(qa, k, bta, mcl)
+    ws = torch.empty(max(pb.pa_workspace_size(dims), 1), dtype=torch.uint8, device="cuda")
+    out_a = torch.empty_like(qa)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    bf = torch.bfloat16
+    x = torch.randn(Bb, h, device="cuda", dtype=bf, generator=g)
+    w_qkv = torch.randn(h, h + 2 * h * H_kv // H_q, device="cuda", dtype=bf, generator=g) * 0.02
+    w_o = torch.randn(h, h, device="cuda", dtype=bf, generator=g) * 0.02
+    w1 = torch.randn(E, h, hi, device="cuda", dtype=bf, generator=g) * 0.02
+    w3 = torch.randn(E, h, hi, device="cuda", dtype=bf, generator=g) * 0.02
+    w2 = torch.randn(E, hi, h, device="cuda", dtype=bf, generator=g) * 0.02
+    te = max(1, Bb * topk // E)  # tokens per expert (balanced synthetic routing)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    res = {}
+
+    def attn(stream):
+        pb.paged_attn(qa, k, v, bta, cla, scale, out_a, dims, ws, stream)
+
+    def gemms():
+        y = x @ w_qkv
+        z = x @ w_o
+        acc = y.float().sum() + z.float().sum()
+        xe = x[:te]
+        for e in range(E):
+            a = xe @ w1[e]
+            c = (torch.nn.functional.silu(a) * (xe @ w3[e])) @ w2[e]
+            acc = acc + c.float().sum()
+        return acc
+
+    def timed(fn_list):
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        cur = torch.cuda.current_stream()
+        t0.record(cur)
+        ends = []
+        for st, fn in fn_list:
+            st.wait_event(t0)
+            with torch.cuda.stream(st):
+                fn(st)
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(st)
+            ends.append(e)
+        for e in ends:
+            cur.wait_event(e)
+        t1.record(cur)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) * 1e3, [t0.elapsed_time(e) * 1e3 for e in ends]
+
+    gout = {}
+    for _ in range(3):  # warm-up (library handles, GEMM kernels)
+        timed([(sa, attn), (sb, lambda st: gout.__setitem__("g", gemms()))])
+    ref = out_a.clone()
+    ga, gb, gc, ca, cb = [], [], [], [], []
+    same = True
+    for _ in range(reps):
+        ga.append(timed([(sa, attn)])[0])
+        gb.append(timed([(sb, lambda st: gout.__setitem__("g", gemms()))])[0])
+        both, ends = timed([(sa, attn), (sb, lambda st: gout.__setitem__("g", gemms()))])
+        gc.append(both)
+        ca.append(ends[0])
+        cb.append(ends[1])
+        same = same and bool(torch.equal(out_a.view(torch.int16), ref.view(torch.int16)))
+    med = lambda a: round(float(np.median(a)), 1)
+    res.update({
+        "partition_alpha_seqs": Ba, "partition_beta_tokens": Bb,
+        "gemm_shapes": {"h": h, "h_i": hi, "experts": E, "top_k": topk, "tokens_per_expert": te},
+        "attn_alone_us": med(ga), "gemm_alone_us": med(gb),
+        "phase_sequential_us": round(med(ga) + med(gb), 1), "phase_overlapped_us": med(gc),
+        "attn_end_in_overlap_us": med(ca), "gemm_end_in_overlap_us": med(cb),
+        "overlap_speedup": round((med(ga) + med(gb)) / med(gc), 3),
+        "attn_slowdown_in_overlap": round(med(ca) / med(ga), 3),
+        "attn_bit_identical_under_overlap": same,
+    })
+    return res
 
 
 def _cpu_model():
