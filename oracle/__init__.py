@@ -56,6 +56,8 @@ def _bind(lib):
     lib.oracle_softmax_weights.restype = ctypes.c_int
     lib.oracle_kv_append.argtypes = [P, P, I32, P, I32, P, P, I32, I32, I32, I32, I32, P, P]
     lib.oracle_kv_append.restype = ctypes.c_int
+    lib.oracle_schedule_step.argtypes = [P] * 10 + [I32] * 5 + [P, P, P, I32, P, P, P]
+    lib.oracle_schedule_step.restype = ctypes.c_int
     lib.oracle_set_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_threads.restype = None
     lib.oracle_get_threads.argtypes = []
@@ -189,3 +191,38 @@ def kv_append(k_new, v_new, block_table, context_lens, k_pages, v_pages, query_s
     if rc != 0:
         raise ValueError(f"oracle_kv_append failed with code {rc}")
     return kp, vp
+
+
+SCHED_FIELDS = ("free_pages", "hdr", "queue_seq", "queue_tok", "queue_fin", "slot_seq", "slot_order",
+                "slot_fin", "context_lens", "block_table")
+
+
+def sched_init(S, P, MP, Q):
+    """Empty scheduler state: all P pages free (stack top = page P-1), empty
+    queue of Q entries, S empty slots of MP block-table entries."""
+    return dict(free_pages=np.arange(P, dtype=np.int32), hdr=np.array([P, 0, 0, 0], np.int32),
+                queue_seq=np.zeros(Q, np.int32), queue_tok=np.zeros(Q, np.int32),
+                queue_fin=np.zeros(Q, np.int32), slot_seq=np.full(S, -1, np.int32),
+                slot_order=np.zeros(S, np.int32), slot_fin=np.zeros(S, np.int32),
+                context_lens=np.zeros(S, np.int32), block_table=np.zeros((S, MP), np.int32))
+
+
+def schedule_step(state, token_budget, new_seq=(), new_prompt=(), new_fin=()):
+    """One scheduler step on a copy of `state` (see oracle_schedule_step).
+    Returns (new state, query_start_loc [S+1], finished ids, info [8])."""
+    st = {k: np.array(state[k], dtype=np.int32, copy=True, order="C") for k in SCHED_FIELDS}
+    S, MP = st["block_table"].shape
+    P, Q = st["free_pages"].shape[0], st["queue_seq"].shape[0]
+    ns = np.ascontiguousarray(new_seq, np.int32)
+    npr = np.ascontiguousarray(new_prompt, np.int32)
+    nf = np.ascontiguousarray(new_fin, np.int32)
+    qsl = np.zeros(S + 1, np.int32)
+    fin_out = np.zeros(S, np.int32)
+    info = np.zeros(8, np.int32)
+    rc = _load().oracle_schedule_step(*[_ptr(st[k]) for k in SCHED_FIELDS], S, P, MP, Q,
+                                      int(token_budget), _ptr(ns) if ns.size else None,
+                                      _ptr(npr) if npr.size else None, _ptr(nf) if nf.size else None,
+                                      int(ns.size), _ptr(qsl), _ptr(fin_out), _ptr(info))
+    if rc != 0:
+        raise ValueError(f"oracle_schedule_step failed with code {rc}")
+    return st, qsl, fin_out[:info[1]].copy(), info

@@ -356,3 +356,164 @@ int oracle_kv_append(const void *k_new, const void *v_new, int32_t elem_bytes,
   }
   return 0;
 }
+
+/* Scheduler step: the GPU-resident page allocator and block-table builder of
+ * the paper's Resource-Aware Scheduler (Sec. 6: a prefill scheduler holding a
+ * queue of waiting sequences and a decode scheduler that estimates the KV
+ * blocks the next token needs, garbage-collects finished sequences and, when
+ * blocks run short, preempts the newest decode sequences, which re-enter the
+ * prefill queue ahead of new arrivals while admission pauses).
+ *
+ * State (updated in place): a stack of free pages free_pages[0 .. hdr[0]-1]
+ * (top = last); hdr = {free count, next admission order, queue head, queue
+ * length}; a circular queue of Q entries (logical id, tokens to prefill,
+ * finish length); per slot: logical id (-1 = empty), admission order, finish
+ * length, context length, block-table row of MP entries.  Pages hold 16
+ * tokens.  One step:
+ *   0. append the arrivals (valid: 1 <= prompt <= finish <= MP*16) at the
+ *      queue tail while the queue keeps S entries free for preemption;
+ *   1. free every slot whose context reached its finish length (its pages are
+ *      pushed in slot order, page order), reporting its id;
+ *   2. a decode slot needs a page iff its context is a multiple of 16;
+ *   3. if more pages are needed than free, preempt the newest decode slots
+ *      (largest admission order) until the rest fit: their pages are pushed
+ *      (slot order) and they re-enter the queue front, lowest slot nearest the
+ *      head, to prefill their whole context again; no admission this step;
+ *   4. each remaining decode slot (slot order) pops its page if it needs one,
+ *      and its context grows by one (this step's token);
+ *   5. otherwise admit queue-head entries in order while their tokens stay
+ *      within token_budget, their pages fit and empty slots remain: the i-th
+ *      admitted takes the i-th lowest empty slot and pops its pages in order;
+ *      its context is the prefilled length;
+ *   6. rows: 1 per decode slot, the prefilled length per admitted slot, 0
+ *      otherwise; query_start_loc[S+1] is their prefix sum.
+ * info = {mode (1 = preemption), finished, preempted, admitted, decode slots,
+ * accepted arrivals, free pages after, total rows}.  Returns 0, or -1 on bad
+ * sizes or a state that is not one the step can produce (a page index out of
+ * range, a context past the table). */
+int oracle_schedule_step(int32_t *free_pages, int32_t *hdr, int32_t *queue_seq, int32_t *queue_tok,
+                         int32_t *queue_fin, int32_t *slot_seq, int32_t *slot_order,
+                         int32_t *slot_fin, int32_t *context_lens, int32_t *block_table,
+                         int32_t S, int32_t P, int32_t MP, int32_t Q, int32_t token_budget,
+                         const int32_t *new_seq, const int32_t *new_prompt, const int32_t *new_fin,
+                         int32_t n_new, int32_t *query_start_loc, int32_t *finished_out,
+                         int32_t *info) {
+  if (!free_pages || !hdr || !queue_seq || !queue_tok || !queue_fin || !slot_seq || !slot_order ||
+      !slot_fin || !context_lens || !block_table || !query_start_loc || !finished_out || !info)
+    return -1;
+  if (S <= 0 || P < 0 || MP <= 0 || Q <= S || token_budget < 0 || n_new < 0) return -1;
+  if (n_new > 0 && (!new_seq || !new_prompt || !new_fin)) return -1;
+  int32_t free_n = hdr[0], head = hdr[2], qlen = hdr[3];
+  if (free_n < 0 || free_n > P || head < 0 || head >= Q || qlen < 0 || qlen > Q) return -1;
+  for (int32_t s = 0; s < S; ++s) {
+    if (slot_seq[s] < 0) continue;
+    const int32_t c = context_lens[s];
+    if (c < 1 || (c + 15) / 16 > MP) return -1;
+    for (int32_t p = 0; p < (c + 15) / 16; ++p) {
+      const int32_t pg = block_table[(int64_t)s * MP + p];
+      if (pg < 0 || pg >= P) return -1;
+    }
+  }
+  for (int i = 0; i < 8; ++i) info[i] = 0;
+  int32_t *rows = (int32_t *)calloc((size_t)S, sizeof(int32_t));
+  char *pre = (char *)calloc((size_t)S, 1);
+  if (!rows || !pre) {
+    free(rows);
+    free(pre);
+    return -2;
+  }
+  /* 0. arrivals */
+  for (int32_t i = 0; i < n_new; ++i) {
+    const int32_t pl = new_prompt[i], fin = new_fin[i];
+    if (pl < 1 || fin < pl || fin > MP * 16 || qlen >= Q - S) continue;
+    const int32_t at = (head + qlen) % Q;
+    queue_seq[at] = new_seq[i];
+    queue_tok[at] = pl;
+    queue_fin[at] = fin;
+    ++qlen;
+    ++info[5];
+  }
+  /* 1. finished slots */
+  for (int32_t s = 0; s < S; ++s) {
+    if (slot_seq[s] < 0 || context_lens[s] < slot_fin[s]) continue;
+    finished_out[info[1]++] = slot_seq[s];
+    for (int32_t p = 0; p < (context_lens[s] + 15) / 16; ++p)
+      free_pages[free_n++] = block_table[(int64_t)s * MP + p];
+    slot_seq[s] = -1;
+    context_lens[s] = 0;
+  }
+  /* 2. pages the decode slots need */
+  int32_t need = 0;
+  for (int32_t s = 0; s < S; ++s)
+    if (slot_seq[s] >= 0 && context_lens[s] % 16 == 0) ++need;
+  /* 3. preemption: newest first until the rest fit */
+  if (need > free_n) {
+    info[0] = 1;
+    int32_t avail = free_n;
+    while (need > avail) {
+      int32_t newest = -1;
+      for (int32_t s = 0; s < S; ++s)
+        if (slot_seq[s] >= 0 && !pre[s] && (newest < 0 || slot_order[s] > slot_order[newest])) newest = s;
+      pre[newest] = 1;
+      avail += (context_lens[newest] + 15) / 16;
+      if (context_lens[newest] % 16 == 0) --need;
+    }
+    int32_t n_pre = 0;
+    for (int32_t s = 0; s < S; ++s) n_pre += pre[s];
+    head = ((head - n_pre) % Q + Q) % Q;
+    int32_t k = 0;
+    for (int32_t s = 0; s < S; ++s) {
+      if (!pre[s]) continue;
+      for (int32_t p = 0; p < (context_lens[s] + 15) / 16; ++p)
+        free_pages[free_n++] = block_table[(int64_t)s * MP + p];
+      const int32_t at = (head + k++) % Q;
+      queue_seq[at] = slot_seq[s];
+      queue_tok[at] = context_lens[s];
+      queue_fin[at] = slot_fin[s];
+      slot_seq[s] = -1;
+      context_lens[s] = 0;
+    }
+    qlen += n_pre;
+    info[2] = n_pre;
+  }
+  /* 4. decode tokens */
+  for (int32_t s = 0; s < S; ++s) {
+    if (slot_seq[s] < 0) continue;
+    if (context_lens[s] % 16 == 0) block_table[(int64_t)s * MP + context_lens[s] / 16] = free_pages[--free_n];
+    context_lens[s] += 1;
+    rows[s] = 1;
+    ++info[4];
+  }
+  /* 5. admission */
+  if (!info[0]) {
+    int32_t tokens = 0;
+    while (qlen > 0) {
+      const int32_t len = queue_tok[head], pages = (len + 15) / 16;
+      int32_t slot = -1;
+      for (int32_t s = 0; s < S && slot < 0; ++s)
+        if (slot_seq[s] < 0 && rows[s] == 0) slot = s;
+      if (slot < 0 || tokens + len > token_budget || pages > free_n) break;
+      for (int32_t j = 0; j < pages; ++j) block_table[(int64_t)slot * MP + j] = free_pages[--free_n];
+      slot_seq[slot] = queue_seq[head];
+      slot_order[slot] = hdr[1]++;
+      slot_fin[slot] = queue_fin[head];
+      context_lens[slot] = len;
+      rows[slot] = len;
+      tokens += len;
+      head = (head + 1) % Q;
+      --qlen;
+      ++info[3];
+    }
+  }
+  /* 6. rows */
+  query_start_loc[0] = 0;
+  for (int32_t s = 0; s < S; ++s) query_start_loc[s + 1] = query_start_loc[s] + rows[s];
+  info[6] = free_n;
+  info[7] = query_start_loc[S];
+  hdr[0] = free_n;
+  hdr[2] = head;
+  hdr[3] = qlen;
+  free(rows);
+  free(pre);
+  return 0;
+}

@@ -48,6 +48,22 @@ MUTANTS = [
      "const size_t src = ((size_t)(row0 + L - 1 - j) * H_kv + g) * row_bytes;"),
     ("append_v_from_k", "(const char *)v_new + src", "(const char *)k_new + src"),
     ("append_decode_skips_nothing", "L = C > 0 ? 1 : 0;\n    }", "L = 1;\n    }"),
+    ("sched_preempts_oldest", "slot_order[s] > slot_order[newest])) newest = s;",
+     "slot_order[s] < slot_order[newest])) newest = s;"),
+    ("sched_need_off_by_one", "if (slot_seq[s] >= 0 && context_lens[s] % 16 == 0) ++need;",
+     "if (slot_seq[s] >= 0 && context_lens[s] % 16 == 1) ++need;"),
+    ("sched_admits_while_preempting", "if (!info[0]) {\n    int32_t tokens = 0;",
+     "if (1) {\n    int32_t tokens = 0;"),
+    ("sched_finished_pages_leak", "/ 16; ++p)\n      free_pages[free_n++] = block_table",
+     "/ 16 - 1; ++p)\n      free_pages[free_n++] = block_table"),
+    ("sched_budget_checked_before_adding", "tokens + len > token_budget", "tokens > token_budget"),
+    ("sched_preempted_queue_reversed", "const int32_t at = (head + k++) % Q;",
+     "const int32_t at = (head + n_pre - 1 - k++) % Q;"),
+    ("sched_arrivals_fill_reserve", "qlen >= Q - S) continue;", "qlen >= Q) continue;"),
+    ("sched_admit_pops_from_bottom", "block_table[(int64_t)slot * MP + j] = free_pages[--free_n];",
+     "block_table[(int64_t)slot * MP + j] = free_pages[P - free_n--];"),
+    ("sched_decode_token_not_counted", "context_lens[s] += 1;\n    rows[s] = 1;",
+     "rows[s] = 1;"),
 ]
 
 

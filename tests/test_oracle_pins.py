@@ -402,3 +402,114 @@ def test_kv_append_rejects_bad_inputs_and_leaves_pools_unchanged():
     kq = np.zeros((int(qsl[-1]), b.num_kv_heads, b.head_dim), np.uint16)
     with pytest.raises(ValueError):
         oracle.kv_append(kq, kq, b.block_table, b.context_lens, b.k_pages, b.v_pages, query_start_loc=qsl)
+
+
+# --- scheduler step: page allocator and block-table builder -----------------
+
+def _read_schedule_fixture():
+    scen, cur = [], None
+    with open(os.path.join(GOLDEN, "schedule_tiny.txt")) as f:
+        for line in f:
+            line = line.split("#", 1)[0].split()
+            if not line:
+                continue
+            key, vals = line[0], [int(x) for x in line[1:] if x.lstrip("-").isdigit()]
+            if key == "scenario":
+                cur = dict(dims=vals, steps=[])
+                scen.append(cur)
+            elif key == "step":
+                cur["steps"].append({})
+            else:
+                cur["steps"][-1][key] = vals
+    return scen
+
+
+def test_schedule_hand_fixture():
+    for sc in _read_schedule_fixture():
+        S, P, MP, Q, budget = sc["dims"]
+        st = oracle.sched_init(S, P, MP, Q)
+        for stp in sc["steps"]:
+            a = np.array(stp["arrivals"], np.int32).reshape(-1, 3)
+            st, qsl, fin, info = oracle.schedule_step(st, budget, a[:, 0], a[:, 1], a[:, 2])
+            assert info.tolist() == stp["info"]
+            assert qsl.tolist() == stp["qsl"]
+            assert st["hdr"].tolist() == stp["hdr"]
+            sl = np.array(stp["slots"]).reshape(-1, 2)
+            assert st["slot_seq"].tolist() == sl[:, 0].tolist()
+            assert st["context_lens"].tolist() == sl[:, 1].tolist()
+            # block-table entries in use, slot-major
+            used = [int(st["block_table"][s, p]) for s in range(S) if st["slot_seq"][s] >= 0
+                    for p in range(-(-int(st["context_lens"][s]) // 16))]
+            assert used == stp["bt"]
+
+
+def _pages_in_use(st):
+    return [(s, int(st["block_table"][s, p])) for s in range(len(st["slot_seq"]))
+            if st["slot_seq"][s] >= 0 for p in range(-(-int(st["context_lens"][s]) // 16))]
+
+
+def test_schedule_invariants_on_random_streams():
+    """Properties every step must keep, checked on random arrival streams with
+    tight page pools (so preemption happens): pages are conserved and never
+    shared, every surviving decode slot gains exactly its token, preemption
+    happens only when pages run short and takes the newest slots, admission
+    follows the queue order, and the rows describe the step."""
+    rng = np.random.default_rng(2)
+    preempted_total = admitted_total = 0
+    for trial in range(10):
+        S, MP, Q = int(rng.integers(3, 9)), 12, 40
+        P = int(rng.integers(S + 2, 4 * S + 4))
+        budget = int(rng.integers(40, 200))
+        st = oracle.sched_init(S, P, MP, Q)
+        next_id = 100
+        expect_queue = []  # logical ids in queue order (model of the queue)
+        for step in range(60):
+            n = int(rng.integers(0, 3))
+            ids = list(range(next_id, next_id + n)); next_id += n
+            pr = rng.integers(1, 40, n)
+            fin = np.minimum(pr + rng.integers(0, 60, n), MP * 16)
+            prev = {k: v.copy() for k, v in st.items()}
+            st, qsl, finished, info = oracle.schedule_step(st, budget, ids, pr, fin)
+            mode, n_fin, n_pre, n_adm, n_dec, n_acc = (int(x) for x in info[:6])
+            expect_queue += ids[:n_acc]
+            # pages: a permutation of 0..P-1 split between free stack and slots
+            used = [p for _, p in _pages_in_use(st)]
+            free = st["free_pages"][:st["hdr"][0]].tolist()
+            assert sorted(used + free) == list(range(P))
+            # finished: exactly the slots that had reached their length
+            was = [s for s in range(S) if prev["slot_seq"][s] >= 0
+                   and prev["context_lens"][s] >= prev["slot_fin"][s]]
+            assert sorted(finished.tolist()) == sorted(int(prev["slot_seq"][s]) for s in was)
+            # survivors gained one token each and kept their earlier pages
+            live = [s for s in range(S) if prev["slot_seq"][s] >= 0 and s not in was]
+            survivors = [s for s in live if st["slot_seq"][s] == prev["slot_seq"][s]
+                         and st["slot_order"][s] == prev["slot_order"][s]]
+            gone = [s for s in live if s not in survivors]
+            assert len(gone) == n_pre and n_dec == len(survivors)
+            for s in survivors:
+                c = int(prev["context_lens"][s])
+                assert st["context_lens"][s] == c + 1
+                assert (st["block_table"][s, :-(-c // 16)] == prev["block_table"][s, :-(-c // 16)]).all()
+                assert qsl[s + 1] - qsl[s] == 1
+            if n_pre:
+                assert mode == 1 and n_adm == 0
+                free_before = int(prev["hdr"][0]) + sum(-(-int(prev["context_lens"][s]) // 16) for s in was)
+                need = sum(1 for s in live if prev["context_lens"][s] % 16 == 0)
+                assert need > free_before
+                # the newest slots went, and without the youngest of them it would not fit
+                assert min(prev["slot_order"][s] for s in gone) > max([prev["slot_order"][s] for s in survivors] or [-1])
+                preempted_total += n_pre
+                expect_queue = [int(prev["slot_seq"][s]) for s in sorted(gone)] + expect_queue
+            # admitted: the queue head, in order, into the lowest empty slots
+            adm = [s for s in range(S) if st["slot_seq"][s] >= 0 and s not in survivors]
+            assert len(adm) == n_adm
+            adm_ids = [int(st["slot_seq"][s]) for s in sorted(adm, key=lambda s: st["slot_order"][s])]
+            assert adm_ids == expect_queue[:n_adm]
+            expect_queue = expect_queue[n_adm:]
+            admitted_total += n_adm
+            assert int(st["hdr"][3]) == len(expect_queue)
+            assert sum(int(st["context_lens"][s]) for s in adm) <= budget
+            for s in adm:
+                assert qsl[s + 1] - qsl[s] == st["context_lens"][s]
+            assert qsl[-1] == info[7] and int(st["hdr"][0]) == info[6]
+    assert preempted_total > 20 and admitted_total > 100, (preempted_total, admitted_total)
