@@ -207,8 +207,9 @@ def sched_init(S, P, MP, Q):
                 context_lens=np.zeros(S, np.int32), block_table=np.zeros((S, MP), np.int32))
 
 
-def schedule_step(state, token_budget, new_seq=(), new_prompt=(), new_fin=()):
-    """One scheduler step on a copy of `state` (see oracle_schedule_step).
+def schedule_step(state, n_real, new_seq=(), new_prompt=(), new_fin=()):
+    """One scheduler step on a copy of `state` (see oracle_schedule_step);
+    n_real is the pass's token capacity (decode rows plus prefill tokens).
     Returns (new state, query_start_loc [S+1], finished ids, info [8])."""
     st = {k: np.array(state[k], dtype=np.int32, copy=True, order="C") for k in SCHED_FIELDS}
     S, MP = st["block_table"].shape
@@ -220,7 +221,7 @@ def schedule_step(state, token_budget, new_seq=(), new_prompt=(), new_fin=()):
     fin_out = np.zeros(S, np.int32)
     info = np.zeros(8, np.int32)
     rc = _load().oracle_schedule_step(*[_ptr(st[k]) for k in SCHED_FIELDS], S, P, MP, Q,
-                                      int(token_budget), _ptr(ns) if ns.size else None,
+                                      int(n_real), _ptr(ns) if ns.size else None,
                                       _ptr(npr) if npr.size else None, _ptr(nf) if nf.size else None,
                                       int(ns.size), _ptr(qsl), _ptr(fin_out), _ptr(info))
     if rc != 0:

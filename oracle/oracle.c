@@ -382,38 +382,47 @@ int oracle_kv_append(const void *k_new, const void *v_new, int32_t elem_bytes,
  *   4. each remaining decode slot (slot order) pops its page if it needs one,
  *      and its context grows by one (this step's token);
  *   5. otherwise admit queue-head entries in order while their tokens stay
- *      within token_budget, their pages fit and empty slots remain: the i-th
+ *      within what the pass has left (n_real, the pipeline's token capacity
+ *      per pass, minus the decode rows of step 4), their pages fit and empty
+ *      slots remain: the i-th
  *      admitted takes the i-th lowest empty slot and pops its pages in order;
  *      its context is the prefilled length;
  *   6. rows: 1 per decode slot, the prefilled length per admitted slot, 0
  *      otherwise; query_start_loc[S+1] is their prefix sum.
  * info = {mode (1 = preemption), finished, preempted, admitted, decode slots,
- * accepted arrivals, free pages after, total rows}.  Returns 0, or -1 on bad
- * sizes or a state that is not one the step can produce (a page index out of
- * range, a context past the table). */
+ * accepted arrivals, free pages after, total rows}.  Returns 0, or -1 (and
+ * changes nothing) on bad sizes or a state that is not one the step can
+ * produce: a page index out of range, a context or finish length past the
+ * table, more pages held and free than the pool has, or more sequences queued
+ * and seated than the queue holds (steps 0 and 3 keep that sum within Q, so
+ * preempted entries always fit). */
 int oracle_schedule_step(int32_t *free_pages, int32_t *hdr, int32_t *queue_seq, int32_t *queue_tok,
                          int32_t *queue_fin, int32_t *slot_seq, int32_t *slot_order,
                          int32_t *slot_fin, int32_t *context_lens, int32_t *block_table,
-                         int32_t S, int32_t P, int32_t MP, int32_t Q, int32_t token_budget,
+                         int32_t S, int32_t P, int32_t MP, int32_t Q, int32_t n_real,
                          const int32_t *new_seq, const int32_t *new_prompt, const int32_t *new_fin,
                          int32_t n_new, int32_t *query_start_loc, int32_t *finished_out,
                          int32_t *info) {
   if (!free_pages || !hdr || !queue_seq || !queue_tok || !queue_fin || !slot_seq || !slot_order ||
       !slot_fin || !context_lens || !block_table || !query_start_loc || !finished_out || !info)
     return -1;
-  if (S <= 0 || P < 0 || MP <= 0 || Q <= S || token_budget < 0 || n_new < 0) return -1;
+  if (S <= 0 || P < 0 || MP <= 0 || Q <= S || n_real < 0 || n_new < 0) return -1;
   if (n_new > 0 && (!new_seq || !new_prompt || !new_fin)) return -1;
   int32_t free_n = hdr[0], head = hdr[2], qlen = hdr[3];
   if (free_n < 0 || free_n > P || head < 0 || head >= Q || qlen < 0 || qlen > Q) return -1;
+  int64_t held = 0, occupied = 0;
   for (int32_t s = 0; s < S; ++s) {
     if (slot_seq[s] < 0) continue;
     const int32_t c = context_lens[s];
-    if (c < 1 || (c + 15) / 16 > MP) return -1;
+    if (c < 1 || slot_fin[s] > MP * 16 || (c + 15) / 16 > MP) return -1;
     for (int32_t p = 0; p < (c + 15) / 16; ++p) {
       const int32_t pg = block_table[(int64_t)s * MP + p];
       if (pg < 0 || pg >= P) return -1;
     }
+    held += (c + 15) / 16;
+    ++occupied;
   }
+  if (free_n + held > P || qlen + occupied > Q) return -1;
   for (int i = 0; i < 8; ++i) info[i] = 0;
   int32_t *rows = (int32_t *)calloc((size_t)S, sizeof(int32_t));
   char *pre = (char *)calloc((size_t)S, 1);
@@ -486,6 +495,7 @@ int oracle_schedule_step(int32_t *free_pages, int32_t *hdr, int32_t *queue_seq, 
   }
   /* 5. admission */
   if (!info[0]) {
+    const int32_t token_budget = n_real - info[4];
     int32_t tokens = 0;
     while (qlen > 0) {
       const int32_t len = queue_tok[head], pages = (len + 15) / 16;

@@ -52,10 +52,12 @@ MUTANTS = [
      "slot_order[s] < slot_order[newest])) newest = s;"),
     ("sched_need_off_by_one", "if (slot_seq[s] >= 0 && context_lens[s] % 16 == 0) ++need;",
      "if (slot_seq[s] >= 0 && context_lens[s] % 16 == 1) ++need;"),
-    ("sched_admits_while_preempting", "if (!info[0]) {\n    int32_t tokens = 0;",
-     "if (1) {\n    int32_t tokens = 0;"),
+    ("sched_admits_while_preempting", "if (!info[0]) {\n    const int32_t token_budget",
+     "if (1) {\n    const int32_t token_budget"),
     ("sched_finished_pages_leak", "/ 16; ++p)\n      free_pages[free_n++] = block_table",
      "/ 16 - 1; ++p)\n      free_pages[free_n++] = block_table"),
+    ("sched_budget_ignores_decode_rows", "const int32_t token_budget = n_real - info[4];",
+     "const int32_t token_budget = n_real;"),
     ("sched_budget_checked_before_adding", "tokens + len > token_budget", "tokens > token_budget"),
     ("sched_preempted_queue_reversed", "const int32_t at = (head + k++) % Q;",
      "const int32_t at = (head + n_pre - 1 - k++) % Q;"),

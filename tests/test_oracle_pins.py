@@ -426,11 +426,11 @@ def _read_schedule_fixture():
 
 def test_schedule_hand_fixture():
     for sc in _read_schedule_fixture():
-        S, P, MP, Q, budget = sc["dims"]
+        S, P, MP, Q, n_real = sc["dims"]
         st = oracle.sched_init(S, P, MP, Q)
         for stp in sc["steps"]:
             a = np.array(stp["arrivals"], np.int32).reshape(-1, 3)
-            st, qsl, fin, info = oracle.schedule_step(st, budget, a[:, 0], a[:, 1], a[:, 2])
+            st, qsl, fin, info = oracle.schedule_step(st, n_real, a[:, 0], a[:, 1], a[:, 2])
             assert info.tolist() == stp["info"]
             assert qsl.tolist() == stp["qsl"]
             assert st["hdr"].tolist() == stp["hdr"]
@@ -459,7 +459,7 @@ def test_schedule_invariants_on_random_streams():
     for trial in range(10):
         S, MP, Q = int(rng.integers(3, 9)), 12, 40
         P = int(rng.integers(S + 2, 4 * S + 4))
-        budget = int(rng.integers(40, 200))
+        n_real = int(rng.integers(40, 200))
         st = oracle.sched_init(S, P, MP, Q)
         next_id = 100
         expect_queue = []  # logical ids in queue order (model of the queue)
@@ -469,7 +469,7 @@ def test_schedule_invariants_on_random_streams():
             pr = rng.integers(1, 40, n)
             fin = np.minimum(pr + rng.integers(0, 60, n), MP * 16)
             prev = {k: v.copy() for k, v in st.items()}
-            st, qsl, finished, info = oracle.schedule_step(st, budget, ids, pr, fin)
+            st, qsl, finished, info = oracle.schedule_step(st, n_real, ids, pr, fin)
             mode, n_fin, n_pre, n_adm, n_dec, n_acc = (int(x) for x in info[:6])
             expect_queue += ids[:n_acc]
             # pages: a permutation of 0..P-1 split between free stack and slots
@@ -508,8 +508,32 @@ def test_schedule_invariants_on_random_streams():
             expect_queue = expect_queue[n_adm:]
             admitted_total += n_adm
             assert int(st["hdr"][3]) == len(expect_queue)
-            assert sum(int(st["context_lens"][s]) for s in adm) <= budget
+            assert sum(int(st["context_lens"][s]) for s in adm) <= n_real - n_dec
+            if not n_pre and st["hdr"][3] > 0:
+                # admission stopped for a reason: the next entry does not fit
+                nxt = int(st["queue_tok"][st["hdr"][2]])
+                empty = sum(1 for s in range(S) if st["slot_seq"][s] < 0)
+                adm_tok = sum(int(st["context_lens"][s]) for s in adm)
+                assert (empty == 0 or adm_tok + nxt > n_real - n_dec
+                        or -(-nxt // 16) > st["hdr"][0])
             for s in adm:
                 assert qsl[s + 1] - qsl[s] == st["context_lens"][s]
             assert qsl[-1] == info[7] and int(st["hdr"][0]) == info[6]
     assert preempted_total > 20 and admitted_total > 100, (preempted_total, admitted_total)
+
+
+def test_schedule_rejects_states_it_cannot_produce():
+    S, P, MP, Q = 2, 4, 2, 4
+    st = oracle.sched_init(S, P, MP, Q)
+    st, *_ = oracle.schedule_step(st, 40, [10, 11], [16, 5], [18, 7])
+    bad = []
+    for field, idx, val in [("block_table", (0, 0), 4), ("block_table", (1, 0), -1),
+                            ("context_lens", 0, 33), ("context_lens", 1, 0), ("slot_fin", 0, 33),
+                            ("hdr", 0, 3), ("hdr", 2, 4), ("hdr", 3, 3)]:
+        t = {k: v.copy() for k, v in st.items()}
+        t[field][idx] = val
+        before = {k: v.copy() for k, v in t.items()}
+        with pytest.raises(ValueError):
+            oracle.schedule_step(t, 40)
+        bad.append(all((before[k] == t[k]).all() for k in t))
+    assert all(bad)
