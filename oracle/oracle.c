@@ -393,7 +393,8 @@ int oracle_kv_append(const void *k_new, const void *v_new, int32_t elem_bytes,
  * accepted arrivals, free pages after, total rows}.  Returns 0, or -1 (and
  * changes nothing) on bad sizes or a state that is not one the step can
  * produce: a page index out of range, a context or finish length past the
- * table, more pages held and free than the pool has, or more sequences queued
+ * table, a queued entry with no tokens or more tokens than its finish length,
+ * more pages held and free than the pool has, or more sequences queued
  * and seated than the queue holds (steps 0 and 3 keep that sum within Q, so
  * preempted entries always fit). */
 int oracle_schedule_step(int32_t *free_pages, int32_t *hdr, int32_t *queue_seq, int32_t *queue_tok,
@@ -423,6 +424,10 @@ int oracle_schedule_step(int32_t *free_pages, int32_t *hdr, int32_t *queue_seq, 
     ++occupied;
   }
   if (free_n + held > P || qlen + occupied > Q) return -1;
+  for (int32_t k = 0; k < qlen; ++k) {
+    const int32_t at = (int32_t)(((int64_t)head + k) % Q);
+    if (queue_tok[at] < 1 || queue_fin[at] < queue_tok[at] || queue_fin[at] > MP * 16) return -1;
+  }
   for (int i = 0; i < 8; ++i) info[i] = 0;
   int32_t *rows = (int32_t *)calloc((size_t)S, sizeof(int32_t));
   char *pre = (char *)calloc((size_t)S, 1);

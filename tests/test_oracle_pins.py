@@ -523,13 +523,15 @@ def test_schedule_invariants_on_random_streams():
 
 
 def test_schedule_rejects_states_it_cannot_produce():
-    S, P, MP, Q = 2, 4, 2, 4
+    S, P, MP, Q = 2, 4, 2, 5
     st = oracle.sched_init(S, P, MP, Q)
-    st, *_ = oracle.schedule_step(st, 40, [10, 11], [16, 5], [18, 7])
+    st, *_ = oracle.schedule_step(st, 40, [10, 11, 12], [16, 5, 3], [18, 7, 4])
+    assert st["hdr"].tolist() == [2, 2, 2, 1]  # id 12 waits at queue entry 2
     bad = []
     for field, idx, val in [("block_table", (0, 0), 4), ("block_table", (1, 0), -1),
                             ("context_lens", 0, 33), ("context_lens", 1, 0), ("slot_fin", 0, 33),
-                            ("hdr", 0, 3), ("hdr", 2, 4), ("hdr", 3, 3)]:
+                            ("hdr", 0, 3), ("hdr", 2, 5), ("hdr", 3, 4), ("queue_tok", 2, 0),
+                            ("queue_fin", 2, 2), ("queue_fin", 2, 33)]:
         t = {k: v.copy() for k, v in st.items()}
         t[field][idx] = val
         before = {k: v.copy() for k, v in t.items()}
