@@ -188,6 +188,9 @@ def main():
     ap.add_argument("--overlap-gemm", action="store_true",
                     help="also measure attention of one half of the batch overlapped with the "
                          "other half's layer GEMMs on a second stream (adds an overlap_gemm object)")
+    ap.add_argument("--sched", action="store_true",
+                    help="also time the scheduler step (pa_schedule_step) in steady state with "
+                         "one slot per sequence of the batch (adds a scheduler object)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -354,11 +357,89 @@ def main():
     if args.overlap_gemm and args.workload in MODEL_GEMMS and qsl is None:
         res["overlap_gemm"] = _overlap_gemm(torch, batch, dev_q, k0, v0, bt, cl, batch.scale,
                                             max(5, min(K, 20)), args.workload)
+    if args.sched:
+        res["scheduler"] = _sched_bench(torch, batch, K, args.seed, not args.no_cpu_baseline)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = _cpu_baseline(batch, args.cpu_baseline_seconds, None)
         res["cpu_baseline"]["host_cpu"] = _cpu_model()
     print(json.dumps(res))
     return 0
+
+
+# scheduler step measurement.
+def _sched_bench(torch, batch, steps, seed, with_cpu):
+    """Steady-state scheduler steps for this batch's shape: one slot per
+    sequence, the batch's page pool, block-table rows long enough for its
+    longest context, and an arrival stream of the MTBench-like mix (Table 4,
+    generation up to 256) at a rate that keeps every slot busy and the queue
+    non-empty.  The arrivals of every step are resident in HBM before timing.
+    Returns the per-step kernel time (HIP events around each launch), the
+    wall-clock steps/s of back-to-back steps, the step's counts, and the
+    oracle's CPU time per step on the same stream as a reported baseline."""
+    S = batch.num_seqs
+    P = int(batch.k_pages.shape[0])
+    MP = max(int(batch.block_table.shape[1]), (450 + 256 + 15) // 16)
+    Q = 4 * S
+    n_real = 4096
+    warm = 300
+    stream_in = W.arrival_stream("mtbench-g256", warm + 2 * steps, 0.1 * S, seed + 77)
+    dev_in = [tuple(to_device(np.ascontiguousarray(x, np.int32), torch) if len(ids) else None
+                    for x in (ids, pr, fn)) + (len(ids),) for ids, pr, fn in stream_in]
+    st = {"free_pages": np.arange(P, dtype=np.int32), "hdr": np.array([P, 0, 0, 0], np.int32),
+          "queue_seq": np.zeros(Q, np.int32), "queue_tok": np.zeros(Q, np.int32),
+          "queue_fin": np.zeros(Q, np.int32), "slot_seq": np.full(S, -1, np.int32),
+          "slot_order": np.zeros(S, np.int32), "slot_fin": np.zeros(S, np.int32),
+          "context_lens": np.zeros(S, np.int32), "block_table": np.zeros((S, MP), np.int32)}
+    arrays = {k: to_device(v, torch) for k, v in st.items()}
+    cst = pb.make_sched_state(arrays)
+    qsl = torch.zeros(S + 1, dtype=torch.int32, device="cuda")
+    fin = torch.zeros(S, dtype=torch.int32, device="cuda")
+    info = torch.zeros((warm + 2 * steps, 8), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def run(i):
+        a, b, c, n = dev_in[i]
+        pb.pa_schedule_step(cst, n_real, a, b, c, n, qsl, fin, info[i], stream)
+
+    for i in range(warm):
+        run(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(warm, warm + steps):
+        run(i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    evs = []
+    for i in range(warm + steps, warm + 2 * steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        run(i)
+        e1.record(stream)
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    us = [a.elapsed_time(b) * 1e3 for a, b in evs]
+    inf = info[warm:].cpu().numpy()
+    res = {"slots": S, "pages": P, "max_pages_per_seq": MP, "queue_cap": Q, "n_real": n_real,
+           "mix": "mtbench-g256", "warmup_steps": warm,
+           "kernel_us_mean": round(float(np.mean(us)), 2),
+           "kernel_us_median": round(float(np.median(us)), 2),
+           "steps_per_s": round(steps / wall, 1), "wall_us_per_step": round(wall / steps * 1e6, 2),
+           "mean_rows": round(float(inf[:, 7].mean()), 1),
+           "mean_decode_slots": round(float(inf[:, 4].mean()), 1),
+           "admitted": int(inf[:, 3].sum()), "finished": int(inf[:, 1].sum()),
+           "preempted": int(inf[:, 2].sum()), "rejected_steps": int((inf[:, 0] < 0).sum())}
+    if with_cpu:
+        import oracle
+        ost = oracle.sched_init(S, P, MP, Q)
+        for ids, pr, fn in stream_in[:warm]:
+            ost, *_ = oracle.schedule_step(ost, n_real, ids, pr, fn)
+        t0 = time.perf_counter()
+        for ids, pr, fn in stream_in[warm:warm + steps]:
+            ost, *_ = oracle.schedule_step(ost, n_real, ids, pr, fn)
+        res["cpu_oracle_us_per_step"] = round((time.perf_counter() - t0) / steps * 1e6, 2)
+        res["cpu_oracle_note"] = ("oracle step incl. its Python marshalling (copies of the state "
+                                  "arrays), one thread")
+    return res
 
 
 # Expert-FFN and projection shapes of the modelled MoE models (model dim h,

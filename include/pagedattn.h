@@ -198,6 +198,95 @@ int pa_kv_append(const void *k_new, const void *v_new, const int32_t *block_tabl
                  const int32_t *context_lens, const int32_t *query_start_loc, void *k_pages,
                  void *v_pages, const pa_dims_t *dims, hipStream_t stream);
 
+/* Scheduler step: the GPU-resident page allocator and block-table builder of
+ * the Resource-Aware Scheduler (Sec. 6.2).  A prefill scheduler holds a queue
+ * of sequences waiting for their prompt pass; a decode scheduler estimates the
+ * 16-token pages its sequences' next tokens need, garbage-collects finished
+ * sequences and, when pages run short, preempts the newest decode sequences,
+ * which re-enter the queue ahead of new arrivals and prefill their whole
+ * context again while admission pauses (preemption mode).  Otherwise the
+ * prefill scheduler admits queue-head sequences while their tokens fit what
+ * the pass has left after the decode rows (normal mode).  Both keep their
+ * state in device memory; one call is one kernel launch.
+ *
+ * State (all int32 device arrays, updated in place; page size 16):
+ *   free_pages   [num_pages]  stack of free page indices, entries
+ *                0 .. hdr[0]-1, top = hdr[0]-1
+ *   hdr          [4]  free count, next admission order, queue head, queue
+ *                length
+ *   queue_seq, queue_tok, queue_fin  [queue_cap]  circular queue from the
+ *                head: logical id, tokens to prefill, finish length
+ *   slot_seq     [num_slots]  logical id in the batch slot, -1 = empty
+ *   slot_order   [num_slots]  admission order (larger = newer)
+ *   slot_fin     [num_slots]  context length at which the sequence finishes
+ *   context_lens [num_slots]  tokens in the cache, counting this pass's
+ *   block_table  [num_slots][max_pages_per_seq]
+ * A fresh state: free_pages = 0 .. num_pages-1, hdr = {num_pages, 0, 0, 0},
+ * slot_seq all -1 (the other arrays any value).  context_lens, block_table
+ * and query_start_loc are the attention calls' arguments for the pass, with
+ * the slot as the sequence index (num_seqs = num_slots): an admitted slot's
+ * chunk is its whole context, a decode slot's chunk is one row.
+ *
+ * One step, in this order (slot order = ascending slot index):
+ *   0. arrivals i = 0 .. n_new-1 (new_seq, new_prompt, new_fin: device
+ *      arrays) with 1 <= new_prompt[i] <= new_fin[i] <= 16*max_pages_per_seq
+ *      join the queue tail in order while the queue length stays below
+ *      queue_cap - num_slots; others are dropped;
+ *   1. slots with context_lens >= slot_fin finish: their ids go to
+ *      finished_out in slot order, their pages are pushed (slot order, page
+ *      order), slot_seq = -1, context_lens = 0;
+ *   2. a remaining slot needs a page iff context_lens % 16 == 0;
+ *   3. if more pages are needed than free: preempt the slots with the
+ *      largest admission orders, the fewest that make the rest fit; push their
+ *      pages (slot order); they enter the queue ahead of the head, lowest slot
+ *      first, with tokens = their context; no admission this step;
+ *   4. each remaining slot (slot order) pops its page if needed, and its
+ *      context grows by 1;
+ *   5. in normal mode admit queue-head entries while the running token sum
+ *      stays <= n_real - (decode slots of step 4), their pages fit the free
+ *      stack and empty slots remain; the r-th admitted takes the r-th lowest
+ *      empty slot, order hdr[1] + r, context = its tokens, and pops its pages
+ *      in page order;
+ *   6. query_start_loc [num_slots + 1] = prefix sum of the rows (1 per decode
+ *      slot, the context per admitted slot, 0 otherwise).
+ * info (device, int32 [8]) = {mode (0 normal, 1 preemption, -1 state
+ * rejected), finished, preempted, admitted, decode slots, arrivals accepted,
+ * free pages after, total rows}.  finished_out has num_slots entries.
+ *
+ * The kernel first checks that the state is one a step can produce: header
+ * fields in range, 1 <= context_lens <= 16*max_pages_per_seq and slot_fin <=
+ * 16*max_pages_per_seq for occupied slots, queued entries with
+ * 1 <= tokens <= finish <= 16*max_pages_per_seq, pages free plus held <=
+ * num_pages, queued plus occupied <= queue_cap.  On failure it writes
+ * info = {-1, 0, ...} and changes nothing else.  Page indices themselves are
+ * only copied, never used as addresses, and are not range-checked; admission
+ * orders of occupied slots must be distinct (every step keeps them so).
+ * Errors (host-side, nothing enqueued): PA_EINVAL (null pointer, num_slots
+ * <= 0, queue_cap <= num_slots, negative sizes, or num_slots *
+ * (max_pages_per_seq + 1) * 16 beyond int32), PA_ENOTSUP (num_slots > 8192),
+ * PA_EHIP. */
+typedef struct {
+  int32_t *free_pages;
+  int32_t *hdr;
+  int32_t *queue_seq;
+  int32_t *queue_tok;
+  int32_t *queue_fin;
+  int32_t *slot_seq;
+  int32_t *slot_order;
+  int32_t *slot_fin;
+  int32_t *context_lens;
+  int32_t *block_table;
+  int32_t num_slots;
+  int32_t num_pages;
+  int32_t max_pages_per_seq;
+  int32_t queue_cap;
+} pa_sched_state_t;
+
+int pa_schedule_step(const pa_sched_state_t *state, int32_t n_real, const int32_t *new_seq,
+                     const int32_t *new_prompt, const int32_t *new_fin, int32_t n_new,
+                     int32_t *query_start_loc, int32_t *finished_out, int32_t *info,
+                     hipStream_t stream);
+
 /* Static description of an error code (never NULL). */
 const char *pa_strerror(int code);
 

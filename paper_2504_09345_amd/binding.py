@@ -21,7 +21,7 @@ PA_BF16, PA_FP32 = 0, 1
 PAGE_SIZE = 16
 
 EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "pa_gather_trace",
-            "pa_kv_append", "pa_strerror")
+            "pa_kv_append", "pa_schedule_step", "pa_strerror")
 
 
 class PaDims(ctypes.Structure):
@@ -36,6 +36,27 @@ class PaTiming(ctypes.Structure):
     """pa_timing_t: three hipEvent_t handles (NULL = not recorded)."""
     _fields_ = [("attn_begin", ctypes.c_void_p), ("attn_end", ctypes.c_void_p),
                 ("reduce_end", ctypes.c_void_p)]
+
+
+SCHED_ARRAYS = ("free_pages", "hdr", "queue_seq", "queue_tok", "queue_fin", "slot_seq",
+                "slot_order", "slot_fin", "context_lens", "block_table")
+
+
+class PaSchedState(ctypes.Structure):
+    """pa_sched_state_t: ten device array pointers, then four sizes."""
+    _fields_ = [(n, ctypes.c_void_p) for n in SCHED_ARRAYS] + [
+        (n, ctypes.c_int32) for n in ("num_slots", "num_pages", "max_pages_per_seq", "queue_cap")]
+
+
+def make_sched_state(arrays) -> PaSchedState:
+    """pa_sched_state_t from a mapping of the ten int32 device arrays (torch
+    tensors or addresses); the sizes come from their shapes."""
+    bt = arrays["block_table"]
+    st = PaSchedState(**{n: _addr(arrays[n]) for n in SCHED_ARRAYS})
+    st.num_slots, st.max_pages_per_seq = int(bt.shape[0]), int(bt.shape[1])
+    st.num_pages = int(arrays["free_pages"].shape[0])
+    st.queue_cap = int(arrays["queue_seq"].shape[0])
+    return st
 
 
 class PagedAttnError(RuntimeError):
@@ -67,6 +88,9 @@ def load():
     lib.pa_gather_trace.restype = ctypes.c_int
     lib.pa_kv_append.argtypes = [P, P, P, P, P, P, P, DP, P]
     lib.pa_kv_append.restype = ctypes.c_int
+    lib.pa_schedule_step.argtypes = [ctypes.POINTER(PaSchedState), ctypes.c_int32, P, P, P,
+                                     ctypes.c_int32, P, P, P, P]
+    lib.pa_schedule_step.restype = ctypes.c_int
     lib.pa_strerror.argtypes = [ctypes.c_int]
     lib.pa_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -181,4 +205,16 @@ def pa_kv_append(k_new, v_new, block_table, context_lens, k_pages, v_pages, dims
                              ctypes.byref(dims), _stream(stream))
     if check and rc != PA_OK:
         raise PagedAttnError("pa_kv_append", rc)
+    return rc
+
+
+def pa_schedule_step(state: PaSchedState, n_real, new_seq, new_prompt, new_fin, n_new,
+                     query_start_loc, finished_out, info, stream=None, check=True) -> int:
+    """int pa_schedule_step(...): one scheduler step on the device-resident state."""
+    rc = load().pa_schedule_step(ctypes.byref(state), int(n_real), _addr(new_seq),
+                                 _addr(new_prompt), _addr(new_fin), int(n_new),
+                                 _addr(query_start_loc), _addr(finished_out), _addr(info),
+                                 _stream(stream))
+    if check and rc != PA_OK:
+        raise PagedAttnError("pa_schedule_step", rc)
     return rc

@@ -2,6 +2,7 @@
 // dispatch.  Validation runs before any HIP call, so a rejected call enqueues
 // nothing and is testable without a GPU.  The library allocates nothing; its
 // only state between calls is the counter that tags each call's range flags.
+#include <climits>
 #include <math.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -388,6 +389,48 @@ int pa_kv_append(const void* k_new, const void* v_new, const int32_t* block_tabl
   a.num_pages = d->num_pages;
   a.max_context_len = d->max_context_len;
   return pa::launch_kv_append(a, stream) == hipSuccess ? PA_OK : PA_EHIP;
+}
+
+int pa_schedule_step(const pa_sched_state_t* state, int32_t n_real, const int32_t* new_seq,
+                     const int32_t* new_prompt, const int32_t* new_fin, int32_t n_new,
+                     int32_t* query_start_loc, int32_t* finished_out, int32_t* info, hipStream_t stream) {
+  if (state == nullptr) return PA_EINVAL;
+  const pa_sched_state_t& st = *state;
+  if (st.num_slots <= 0 || st.num_pages < 0 || st.max_pages_per_seq <= 0 || st.queue_cap <= st.num_slots ||
+      n_real < 0 || n_new < 0)
+    return PA_EINVAL;
+  if (st.num_slots > pa::kSchedMaxSlots) return PA_ENOTSUP;
+  // token and page counts of a step stay within int32
+  if ((int64_t)st.num_slots * (st.max_pages_per_seq + 1) * 16 > INT32_MAX) return PA_EINVAL;
+  if (!st.free_pages && st.num_pages > 0) return PA_EINVAL;
+  if (!st.hdr || !st.queue_seq || !st.queue_tok || !st.queue_fin || !st.slot_seq || !st.slot_order ||
+      !st.slot_fin || !st.context_lens || !st.block_table || !query_start_loc || !finished_out || !info)
+    return PA_EINVAL;
+  if (n_new > 0 && (!new_seq || !new_prompt || !new_fin)) return PA_EINVAL;
+  pa::SchedArgs a;
+  a.free_pages = st.free_pages;
+  a.hdr = st.hdr;
+  a.queue_seq = st.queue_seq;
+  a.queue_tok = st.queue_tok;
+  a.queue_fin = st.queue_fin;
+  a.slot_seq = st.slot_seq;
+  a.slot_order = st.slot_order;
+  a.slot_fin = st.slot_fin;
+  a.context_lens = st.context_lens;
+  a.block_table = st.block_table;
+  a.S = st.num_slots;
+  a.P = st.num_pages;
+  a.MP = st.max_pages_per_seq;
+  a.Q = st.queue_cap;
+  a.n_real = n_real;
+  a.new_seq = new_seq;
+  a.new_prompt = new_prompt;
+  a.new_fin = new_fin;
+  a.n_new = n_new;
+  a.query_start_loc = query_start_loc;
+  a.finished_out = finished_out;
+  a.info = info;
+  return pa::launch_sched(a, stream) == hipSuccess ? PA_OK : PA_EHIP;
 }
 
 const char* pa_strerror(int code) {

@@ -278,3 +278,38 @@ def permute_pages(batch: Batch, seed: int) -> Batch:
                  block_table=bt.astype(np.int32), context_lens=batch.context_lens,
                  query_start_loc=batch.query_start_loc, scale=batch.scale, seed=batch.seed,
                  poison=batch.poison, meta=dict(batch.meta))
+
+
+# --- request arrival streams (scheduler inputs) -----------------------------
+# Prompt and generation lengths of the paper's evaluation workloads (Table 4):
+# (average prompt, maximum prompt, maximum generation).  Prompts are drawn
+# lognormal with sigma 0.8 around a median chosen so the unclipped mean is the
+# average, then clipped to [1, maximum]; generation lengths are uniform in
+# [1, maximum generation].  Synthetic stand-ins: no benchmark item is used.
+ARRIVAL_MIXES = {
+    "mtbench-g32": (98, 450, 32),
+    "mtbench-g128": (98, 450, 128),
+    "mtbench-g256": (98, 450, 256),
+    "rag": (926, 1843, 128),
+    "aime": (128, 410, 512),
+    "tiny": (20, 60, 40),  # small pools for tests that need preemption often
+}
+
+
+def arrival_stream(mix: str, steps: int, per_step: float, seed: int, first_id: int = 0):
+    """Arrivals for `steps` scheduler steps: a Poisson(per_step) count per step,
+    each arrival (logical id, prompt tokens, finish length = prompt +
+    generation).  Returns a list of (ids, prompts, finishes) int32 arrays."""
+    avg, pmax, gmax = ARRIVAL_MIXES[mix]
+    rng = np.random.default_rng(seed)
+    sigma = 0.8
+    med = avg / math.exp(sigma * sigma / 2)
+    out, nid = [], first_id
+    for _ in range(steps):
+        n = int(rng.poisson(per_step))
+        p = _draw_lengths(("lognormal", med, sigma, 1, pmax), n, rng)
+        g = rng.integers(1, gmax, size=n, endpoint=True)
+        ids = np.arange(nid, nid + n, dtype=np.int32)
+        nid += n
+        out.append((ids, p.astype(np.int32), (p + g).astype(np.int32)))
+    return out

@@ -270,3 +270,48 @@ def test_kv_append_without_rows_touches_nothing():
     assert lib.pa_kv_append(None, None, None, None, None, None, None, ctypes.byref(d), None) == pb.PA_OK
     d = dims(num_q_rows=0)
     assert lib.pa_kv_append(None, None, None, None, FAKE, None, None, ctypes.byref(d), None) == pb.PA_OK
+
+
+def _sched_state(S=4, P=8, MP=2, Q=8):
+    st = pb.PaSchedState(**{n: FAKE for n in pb.SCHED_ARRAYS})
+    st.num_slots, st.num_pages, st.max_pages_per_seq, st.queue_cap = S, P, MP, Q
+    return st
+
+
+@host_only
+@pytest.mark.parametrize("case", ["null_state", "null_hdr", "null_info", "no_slots", "queue_small",
+                                  "neg_pages", "no_table", "neg_budget", "neg_arrivals",
+                                  "null_arrivals", "too_many_slots", "int32_range"])
+def test_schedule_step_validation(case):
+    import ctypes
+    st = _sched_state()
+    args = dict(n_real=64, ns=FAKE, npr=FAKE, nf=FAKE, n_new=2, qsl=FAKE, fin=FAKE, info=FAKE)
+    expect = pb.PA_EINVAL
+    if case == "null_hdr":
+        st.hdr = None
+    elif case == "null_info":
+        args["info"] = None
+    elif case == "no_slots":
+        st.num_slots = 0
+    elif case == "queue_small":
+        st.queue_cap = st.num_slots
+    elif case == "neg_pages":
+        st.num_pages = -1
+    elif case == "no_table":
+        st.max_pages_per_seq = 0
+    elif case == "neg_budget":
+        args["n_real"] = -1
+    elif case == "neg_arrivals":
+        args["n_new"] = -1
+    elif case == "null_arrivals":
+        args["npr"] = None
+    elif case == "too_many_slots":
+        st.num_slots, st.queue_cap = 8193, 9000
+        expect = pb.PA_ENOTSUP
+    elif case == "int32_range":
+        st.num_slots, st.queue_cap, st.max_pages_per_seq = 4096, 5000, 1 << 16
+    lib = pb.load()
+    rc = lib.pa_schedule_step(None if case == "null_state" else ctypes.byref(st), args["n_real"],
+                              args["ns"], args["npr"], args["nf"], args["n_new"], args["qsl"],
+                              args["fin"], args["info"], None)
+    assert rc == expect
