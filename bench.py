@@ -191,6 +191,10 @@ def main():
     ap.add_argument("--sched", action="store_true",
                     help="also time the scheduler step (pa_schedule_step) in steady state with "
                          "one slot per sequence of the batch (adds a scheduler object)")
+    ap.add_argument("--perf-model", action="store_true",
+                    help="also evaluate the paper's performance model (pa_perf_model) for an "
+                         "MI355X-hosted KV cache, fed with this run's attention bandwidth and a "
+                         "measured host-to-device copy rate (adds a perf_model object)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -359,6 +363,8 @@ def main():
                                             max(5, min(K, 20)), args.workload)
     if args.sched:
         res["scheduler"] = _sched_bench(torch, batch, K, args.seed, not args.no_cpu_baseline)
+    if args.perf_model:
+        res["perf_model"] = _perf_model_leg(torch, achieved * 1e9)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = _cpu_baseline(batch, args.cpu_baseline_seconds, None)
         res["cpu_baseline"]["host_cpu"] = _cpu_model()
@@ -440,6 +446,58 @@ def _sched_bench(torch, batch, steps, seed, with_cpu):
         res["cpu_oracle_note"] = ("oracle step incl. its Python marshalling (copies of the state "
                                   "arrays), one thread")
     return res
+
+
+# performance model for an MI355X-hosted KV cache.
+MI355X_BF16_FLOPS = 2.5e15  # dense bf16 matrix peak
+MI355X_HBM_BYTES = 288e9
+
+
+def _perf_model_leg(torch, attn_bw):
+    """The paper's Sec. 5 model (Eqs. 1-14) with the KV cache and its attention
+    on one MI355X: Mixtral-8x7B (94 GB of bf16 weights, Sec. 7) streamed from
+    host memory once per iteration at the measured pinned host-to-device rate
+    (B_IO, measured as the paper did, with 1 GiB transfers), the KV cache in
+    HBM (288 GB less 32 GB kept for activations and the weight window), the
+    attention read rate measured by this run, MTBench-like lengths (p = 98,
+    g = 32 and 128) with 16-token blocks, and the request batch K = 5 g q of
+    the paper's evaluation."""
+    n = 1 << 30
+    host = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    dev = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dev.copy_(host, non_blocking=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        dev.copy_(host, non_blocking=True)
+    e1.record()
+    torch.cuda.synchronize()
+    b_io = reps * n / (e0.elapsed_time(e1) / 1e3)
+    del host, dev
+    base = dict(num_experts=8, top_k=2, model_dim=4096, expert_dim=14336, gqa_group=4,
+                model_bytes=94e9, kv_bytes_per_token=131072, gemm_flops=MI355X_BF16_FLOPS,
+                io_bw=b_io, kv_capacity_bytes=MI355X_HBM_BYTES - 32e9, attn_bw=attn_bw,
+                attn_intensity=1.0, batch=1.0, prompt=98, block=16)
+    out = {"model": "mixtral-8x7b", "io_bw_measured_gb_s": round(b_io / 1e9, 2),
+           "attn_bw_measured_gb_s": round(attn_bw / 1e9, 1), "kv_capacity_gb": 256.0,
+           "gemm_tflops": MI355X_BF16_FLOPS / 1e12, "cases": []}
+    for g in (32, 128):
+        q = pb.pa_perf_model(**dict(base, gen=g))["q"]
+        r = pb.pa_perf_model(**dict(base, gen=g, batch=5 * g * q))
+        out["cases"].append({
+            "prompt": 98, "gen": g, "batch_K": round(5 * g * q),
+            "tokens_to_saturate": round(r["tokens_to_saturate"]), "delta_s": round(r["delta"], 3),
+            "kv_tokens": round(r["kv_tokens"]), "pme": round(r["pme"], 6),
+            "t_gpu_tok_s": round(r["t_gpu"], 1), "t_max_tok_s": round(r["t_max"], 1),
+            "stage1_gpu_util": round(r["t_max"] / r["t_gpu"], 4),
+            "q": round(r["q"], 2), "decode_seqs": round(r["decode_seqs"], 1),
+            "t1_tok_s": round(r["t1"], 1), "t2_tok_s": round(r["t2"], 1), "t_tok_s": round(r["t"], 1),
+            "kv_bw_needed_gb_s": round(r["kv_bw"] / 1e9, 2),
+            "attn_headroom": round(r["attn_headroom"], 1),
+            "t_with_measured_attention_tok_s": round(r["t_attn_bound"], 1)})
+    return out
 
 
 # Expert-FFN and projection shapes of the modelled MoE models (model dim h,

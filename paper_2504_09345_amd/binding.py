@@ -21,7 +21,7 @@ PA_BF16, PA_FP32 = 0, 1
 PAGE_SIZE = 16
 
 EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "pa_gather_trace",
-            "pa_kv_append", "pa_schedule_step", "pa_strerror")
+            "pa_kv_append", "pa_schedule_step", "pa_perf_model", "pa_strerror")
 
 
 class PaDims(ctypes.Structure):
@@ -59,6 +59,26 @@ def make_sched_state(arrays) -> PaSchedState:
     return st
 
 
+PM_INPUT_DOUBLES = ("num_experts", "top_k", "model_dim", "expert_dim", "gqa_group", "model_bytes",
+                    "kv_bytes_per_token", "gemm_flops", "io_bw", "kv_capacity_bytes", "attn_bw",
+                    "attn_intensity", "batch")
+PM_INPUT_INTS = ("prompt", "gen", "block")
+PM_OUTPUTS = ("intensity_per_token", "tokens_to_saturate", "pme", "delta", "kv_tokens", "t_gpu",
+              "t_max", "mem_bw", "kv_bw", "attn_flops", "kv_effective", "kv_blocks", "q",
+              "decode_seqs", "t1", "t_prefill", "iterations", "t2", "t", "attn_headroom",
+              "delta_eff", "t_attn_bound")
+
+
+class PaPmInput(ctypes.Structure):
+    """pa_pm_input_t (include/pa_perf_model.h)"""
+    _fields_ = [(n, ctypes.c_double) for n in PM_INPUT_DOUBLES] + [(n, ctypes.c_int32) for n in PM_INPUT_INTS]
+
+
+class PaPmOutput(ctypes.Structure):
+    """pa_pm_output_t"""
+    _fields_ = [(n, ctypes.c_double) for n in PM_OUTPUTS]
+
+
 class PagedAttnError(RuntimeError):
     def __init__(self, fn, code):
         super().__init__(f"{fn} returned {code}: {pa_strerror(code)}")
@@ -91,6 +111,8 @@ def load():
     lib.pa_schedule_step.argtypes = [ctypes.POINTER(PaSchedState), ctypes.c_int32, P, P, P,
                                      ctypes.c_int32, P, P, P, P]
     lib.pa_schedule_step.restype = ctypes.c_int
+    lib.pa_perf_model.argtypes = [ctypes.POINTER(PaPmInput), ctypes.POINTER(PaPmOutput)]
+    lib.pa_perf_model.restype = ctypes.c_int
     lib.pa_strerror.argtypes = [ctypes.c_int]
     lib.pa_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -218,3 +240,18 @@ def pa_schedule_step(state: PaSchedState, n_real, new_seq, new_prompt, new_fin, 
     if check and rc != PA_OK:
         raise PagedAttnError("pa_schedule_step", rc)
     return rc
+
+
+def pa_perf_model(**inputs) -> dict:
+    """int pa_perf_model(...): the Sec. 5 performance model for one
+    configuration; keyword names are the pa_pm_input_t fields (missing ones
+    are 0).  Returns the pa_pm_output_t fields as a dict."""
+    unknown = set(inputs) - set(PM_INPUT_DOUBLES) - set(PM_INPUT_INTS)
+    if unknown:
+        raise TypeError(f"unknown inputs {sorted(unknown)}")
+    x = PaPmInput(**inputs)
+    o = PaPmOutput()
+    rc = load().pa_perf_model(ctypes.byref(x), ctypes.byref(o))
+    if rc != PA_OK:
+        raise PagedAttnError("pa_perf_model", rc)
+    return {n: getattr(o, n) for n in PM_OUTPUTS}
