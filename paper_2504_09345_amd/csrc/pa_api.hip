@@ -11,6 +11,7 @@
 #include <chrono>
 
 #include "pa_kernels.h"
+#include "pa_sched.h"
 #include "pagedattn.h"
 
 namespace {

@@ -41,6 +41,7 @@
 
 #include "pa_device.h"
 #include "pa_kernels.h"
+#include "pa_sched.h"
 
 namespace pa {
 
