@@ -21,7 +21,13 @@ namespace {
 constexpr int kDefaultPagesPerSplit = 128;
 
 // Share of the CUs that run the persistent stream-K decode grid.
-constexpr int kStreamCuNum = 3, kStreamCuDen = 4;
+#ifndef PA_STREAM_CU_NUM
+#define PA_STREAM_CU_NUM 13
+#endif
+#ifndef PA_STREAM_CU_DEN
+#define PA_STREAM_CU_DEN 16
+#endif
+constexpr int kStreamCuNum = PA_STREAM_CU_NUM, kStreamCuDen = PA_STREAM_CU_DEN;
 
 struct Plan {
   int s = 0;
@@ -165,10 +171,12 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
       return PA_EHIP;
     const int per_cu = pa::stream_occupancy(dims->dtype, dims->head_dim, p.s, p.W);
     if (per_cu <= 0) return PA_EHIP;
-    // Three quarters of the CUs stream faster than all of them (Mixtral
-    // batch 256: 208 vs 216 us; DBRX 469 vs 490 us; 32k contexts 746 vs
-    // 766 us, on MI355X): fewer requests in flight keep HBM in its efficient
-    // range and even out the per-XCD rates.
+    // 13/16 of the CUs (208 of 256 on MI355X, 26 per XCD) stream faster than
+    // all of them: fewer requests in flight keep HBM in its efficient range.
+    // Back-to-back launches (measured as a sustained loop, MI355X): Mixtral
+    // batch 256 213-214 us per launch at 208 workgroups, 214-217 at 192, 218
+    // at 256, 231 at 160; DBRX and 32k contexts within 0.5 % from 192 to 208,
+    // 1-2 % slower at 256.
     int64_t g = (int64_t)per_cu * cus * kStreamCuNum / kStreamCuDen;
     if (g < 1) g = 1;
     if (g < p.g_min) g = p.g_min;
@@ -240,11 +248,13 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     pf.H_kv = dims->num_kv_heads;
     pf.max_context_len = dims->max_context_len;
     if (mixed) {
-      // the CUs the decode grid leaves free (at least a quarter of them)
+      // a quarter of the CUs for the chunks, the rest (at most the decode
+      // grid) for the decode rows: one grid of one workgroup per CU
       // (measured on the mixed Mixtral batch: splits 176..208 / 48..80 of the
-      // 256 CUs are within 2 % of this one)
-      const int g_pf = cus - G > cus / 4 ? cus - G : (cus / 4 > 0 ? cus / 4 : 1);
-      e = pa::launch_mixed(p.s, sa, pf, G, G + g_pf, stream, next_events());
+      // 256 CUs are within 2 % of 192 / 64)
+      const int g_pf = cus / 4 > 0 ? cus / 4 : 1;
+      const int g_dec = G < cus - g_pf ? G : (cus - g_pf > p.g_min ? cus - g_pf : (int)p.g_min);
+      e = pa::launch_mixed(p.s, sa, pf, g_dec, g_dec + g_pf, stream, next_events());
     } else {
       const int per_cu = pa::prefill_occupancy(p.s, dims->num_seqs);
       if (per_cu <= 0) return PA_EHIP;
