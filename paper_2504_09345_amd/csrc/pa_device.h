@@ -154,21 +154,28 @@ template <int G> __device__ __forceinline__ float across_groups_sum(float v) {
 }
 
 // Exclusive prefix sum of one value per thread over a workgroup of NT
-// threads (Hillis-Steele in LDS; s_tmp holds NT ints).
+// threads: an inclusive scan inside each wave (lane shuffles), one LDS round
+// for the wave totals (s_tmp holds NT / 64 ints), two barriers.
 template <int NT>
 __device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp) {
-  const int tid = threadIdx.x;
-  s_tmp[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < NT; off <<= 1) {
-    const int add = tid >= off ? s_tmp[tid - off] : 0;
-    __syncthreads();
-    s_tmp[tid] += add;
-    __syncthreads();
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int t = __shfl_up(x, off, 64);
+    if (lane >= off) x += t;
   }
-  const int incl = s_tmp[tid];
-  __syncthreads();
-  return incl - v;
+  if constexpr (NT <= 64) {
+    return x - v;
+  } else {
+    if (lane == 63) s_tmp[wv] = x;
+    __syncthreads();
+    int before = 0;
+#pragma unroll
+    for (int i = 0; i < NT / 64; ++i) before += i < wv ? s_tmp[i] : 0;
+    __syncthreads();  // s_tmp may be rewritten by the caller next
+    return before + x - v;
+  }
 }
 
 // Block-table address function.  Token t of sequence b sits in slot t % 16 of

@@ -82,6 +82,10 @@ struct StreamSmem {
   __attribute__((aligned(16))) uint8_t kv[MF ? W : 1][MF ? 2 * mfma::kTile : 16];  // per-wave tile staging
 };
 
+// Codes in s_tail for rows without units (a row with units holds 1 .. 16,
+// the tokens in its last page).
+constexpr uint8_t kRowZeros = 0x20, kRowNaN = 0x40;
+
 // The stream-K decode workgroup `bid` of a grid of G (see pa_stream.hip).
 template <typename T, int D, int S, int W, int NBUF, bool MF>
 __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, MF>& sm, int bid, int G_) {
@@ -103,10 +107,13 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
     int local = 0;
     for (int r = r0; r < r1; ++r) {
       int row, nv;
-      int np = seq_decode_row(a.query_start_loc, a.context_lens, a.max_context_len, r, row, nv) == 1
-                   ? (nv + kPage - 1) / kPage : 0;
-      if (np > (int)a.bt_stride) np = 0;  // contract violation: a NaN row (below)
-      s_tail[r] = (uint8_t)(np ? nv - (np - 1) * kPage : 0);
+      const int status = seq_decode_row(a.query_start_loc, a.context_lens, a.max_context_len, r, row, nv);
+      int np = status == 1 ? (nv + kPage - 1) / kPage : 0;
+      const bool bad = status < 0 || np > (int)a.bt_stride;  // contract violation: a NaN row (below)
+      if (bad) np = 0;
+      // tokens in the last page, or for a row without units what its output
+      // gets: kRowZeros (empty decode context), kRowNaN (violation), 0 (none)
+      s_tail[r] = (uint8_t)(np ? nv - (np - 1) * kPage : bad ? kRowNaN : status == 1 ? kRowZeros : 0);
       s_cum[r] = local;
       local += np;
     }
@@ -118,13 +125,14 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
   const int64_t U = (int64_t)a.nb * s_cum[R];
   const int64_t G = G_;
   // Rows without units: zeros for an empty decode context, NaN for a contract
-  // violation; rows r = bid (mod G) are this workgroup's to write.
+  // violation (flagged in s_tail above); rows r = bid (mod G) are this
+  // workgroup's to write.
   for (int r = bid; r < R; r += G_) {
-    int qrow, nv;
-    const int status = seq_decode_row(a.query_start_loc, a.context_lens, a.max_context_len, r, qrow, nv);
-    const int np = status == 1 ? (nv + kPage - 1) / kPage : 0;
-    if (status == 0 || (status == 1 && np > 0 && np <= (int)a.bt_stride)) continue;
-    const float fill = (status < 0 || np > (int)a.bt_stride) ? NAN : 0.0f;
+    if (s_cum[r + 1] != s_cum[r]) continue;  // the row has units
+    const int code = s_tail[r];
+    if (code != kRowZeros && code != kRowNaN) continue;
+    const int qrow = a.query_start_loc != nullptr ? a.query_start_loc[r] : r;
+    const float fill = code == kRowNaN ? NAN : 0.0f;
     T* o = reinterpret_cast<T*>(a.out) + (int64_t)qrow * a.H_q * D;
     for (int i = tid; i < a.H_q * D; i += NT) store_out<T>(o + i, fill);
   }
