@@ -153,18 +153,27 @@ template <int G> __device__ __forceinline__ float across_groups_sum(float v) {
   }
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave, on the VALU's DPP
+// lane paths: shifts by 1, 2, 4, 8 inside each 16-lane row (lanes shifted in
+// from outside the row read 0), then lane 15 of rows 0 and 2 added into rows
+// 1 and 3 (row_bcast:15), then lane 31 into rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
+
 // Exclusive prefix sum of one value per thread over a workgroup of NT
-// threads: an inclusive scan inside each wave (lane shuffles), one LDS round
-// for the wave totals (s_tmp holds NT / 64 ints), two barriers.
+// threads: an inclusive scan inside each wave, one LDS round for the wave
+// totals (s_tmp holds NT / 64 ints), two barriers.
 template <int NT>
 __device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  int x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int t = __shfl_up(x, off, 64);
-    if (lane >= off) x += t;
-  }
+  const int x = wave_incl_scan(v);
   if constexpr (NT <= 64) {
     return x - v;
   } else {

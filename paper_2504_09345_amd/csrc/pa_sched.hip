@@ -29,7 +29,7 @@
 //
 // Mapping: one workgroup of 1024 threads; thread t owns the K consecutive
 // slots t*K .. t*K+K-1 in registers.  Each ordered step is a block-wide
-// prefix sum over the threads (wave shuffles + one LDS round), and the page
+// prefix sum over the threads (DPP lane scans + one LDS round), and the page
 // moves of a step (a variable number of pages per sequence) are flattened:
 // every thread takes page f, f + 1024, ... of the step's total and finds its
 // sequence by binary search over the step's page prefix in LDS.  The
@@ -60,16 +60,6 @@ struct SchedSmem {
   int32_t pref[kSchedMaxSlots + 1];  // page prefix of the moved sequences
 };
 
-__device__ __forceinline__ int wave_incl(int v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int t = __shfl_up(v, off, 64);
-    if (lane >= off) v += t;
-  }
-  return v;
-}
-
 // Block-wide exclusive prefix sum of four counters; `round` alternates the
 // LDS buffer so one barrier per call suffices (a buffer is rewritten two
 // calls later, after every thread has passed the barrier of the call in
@@ -78,7 +68,7 @@ struct Scanner {
   SchedSmem& sm;
   int round;
   __device__ I4 scan(I4 v, I4& total) {
-    const I4 inc{wave_incl(v.x), wave_incl(v.y), wave_incl(v.z), wave_incl(v.w)};
+    const I4 inc{wave_incl_scan(v.x), wave_incl_scan(v.y), wave_incl_scan(v.z), wave_incl_scan(v.w)};
     const int w = threadIdx.x >> 6;
     int(*buf)[4] = sm.wave[round & 1];
     ++round;
@@ -184,6 +174,32 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
     ctx[i] = in ? a.context_lens[s] : 0;
     rows[i] = 0;
   }
+  // Loads that depend on nothing the step computes are issued now, beside the
+  // state: the first chunk of arrivals, and the queue entries j = t*K .. t*K+K-1
+  // (validation reads every queued entry; admission takes the head ones)
+  const int qlen0 = qlen;
+  const bool hdr_in = head >= 0 && head < Q && qlen >= 0 && qlen <= Q;
+  int a_pl = 0, a_fl = 0, a_id = 0;
+  if (tid < a.n_new) {
+    a_pl = a.new_prompt[tid];
+    a_fl = a.new_fin[tid];
+    a_id = a.new_seq[tid];
+  }
+  // (up to two slots per thread: more would spill registers; larger grids
+  // read the entries where they are used)
+  constexpr bool kPre = K <= 2;
+  int qtk[K], qfn[K], qid[K];
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    const int j = tid * K + i;
+    qtk[i] = qfn[i] = qid[i] = 0;
+    if (kPre && hdr_in && j < qlen) {
+      const int q = ring((int64_t)head + j, Q);
+      qtk[i] = a.queue_tok[q];
+      qfn[i] = a.queue_fin[q];
+      qid[i] = a.queue_seq[q];
+    }
+  }
 
   // --- the state must be one a step can produce --------------------------
   const bool hdr_bad = free_n < 0 || free_n > a.P || head < 0 || head >= Q || qlen < 0 || qlen > Q;
@@ -197,7 +213,12 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
       ++occ;
     }
     if (!hdr_bad) {
-      for (int k = tid; k < qlen; k += kSchedThreads) {
+      if constexpr (kPre) {
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+          if (tid * K + i < qlen && (qtk[i] < 1 || qfn[i] < qtk[i] || qfn[i] > max_tokens)) bad = 1;
+      }
+      for (int k = (kPre ? K * kSchedThreads : 0) + tid; k < qlen; k += kSchedThreads) {  // not prefetched
         const int q = ring((int64_t)head + k, Q);
         const int tk = a.queue_tok[q], fq = a.queue_fin[q];
         if (tk < 1 || fq < tk || fq > max_tokens) bad = 1;
@@ -219,17 +240,24 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
   int valid_total = 0;
   for (int base = 0; base < a.n_new; base += kSchedThreads) {
     const int i = base + tid;
-    int ok = 0, pl = 0, fl = 0;
+    int ok = 0, pl = 0, fl = 0, id = 0;
     if (i < a.n_new) {
-      pl = a.new_prompt[i];
-      fl = a.new_fin[i];
+      if (base == 0) {
+        pl = a_pl;
+        fl = a_fl;
+        id = a_id;
+      } else {
+        pl = a.new_prompt[i];
+        fl = a.new_fin[i];
+        id = a.new_seq[i];
+      }
       ok = pl >= 1 && fl >= pl && fl <= max_tokens;
     }
     I4 t;
     const int r = valid_total + sc.scan(I4{ok, 0, 0, 0}, t).x;
     if (ok && r < cap) {
       const int q = ring((int64_t)head + qlen + r, Q);
-      a.queue_seq[q] = a.new_seq[i];
+      a.queue_seq[q] = id;
       a.queue_tok[q] = pl;
       a.queue_fin[q] = fl;
     }
@@ -239,7 +267,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
   qlen += accepted;
 
   // --- 1. finished slots, 2. page demand ----------------------------------
-  int n_fin, need, live;
+  int n_fin, need, live, need_before;  // need_before: needers in earlier threads
   {
     int nf = 0, pf = 0, nd = 0, nl = 0;
 #pragma unroll
@@ -255,6 +283,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
     }
     I4 t;
     const I4 ex = sc.scan(I4{nf, pf, nd, nl}, t);
+    need_before = ex.z;
     int r = ex.x, pr = ex.y;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
@@ -349,11 +378,17 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
 
   // --- 4. decode tokens -----------------------------------------------------
   {
-    int nd = 0;
+    // ranks among the slots that open a page: the garbage-collection scan's,
+    // unless preemption removed some of those slots
+    int k = need_before, n_need = need;
+    if (mode == 1) {  // workgroup-uniform
+      int nd = 0;
 #pragma unroll
-    for (int i = 0; i < K; ++i) nd += seq[i] >= 0 && ctx[i] % kPage == 0;
-    I4 t;
-    int k = sc.scan(I4{nd, 0, 0, 0}, t).x;
+      for (int i = 0; i < K; ++i) nd += seq[i] >= 0 && ctx[i] % kPage == 0;
+      I4 t;
+      k = sc.scan(I4{nd, 0, 0, 0}, t).x;
+      n_need = t.x;
+    }
 #pragma unroll
     for (int i = 0; i < K; ++i) {
       if (seq[i] < 0) continue;
@@ -366,7 +401,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
       a.context_lens[s] = ctx[i];
       rows[i] = 1;
     }
-    free_n -= t.x;  // == need
+    free_n -= n_need;
   }
   const int n_dec = live;
 
@@ -393,12 +428,22 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
     }
     const int m = min(qlen, te.x);
     // candidates j = tid*K + i < m, in queue order from the head
+    // (entries not prefetched, such as this step's arrivals, written before
+    // the garbage-collection barrier, are read here)
     int tk[K];
     int st = 0, sp = 0;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
       const int j = tid * K + i;
-      tk[i] = j < m ? a.queue_tok[ring((int64_t)head + j, Q)] : 0;
+      if (j < m && (!kPre || j >= qlen0)) {
+        const int q = ring((int64_t)head + j, Q);
+        qtk[i] = a.queue_tok[q];
+        if constexpr (kPre) {
+          qfn[i] = a.queue_fin[q];
+          qid[i] = a.queue_seq[q];
+        }
+      }
+      tk[i] = j < m ? qtk[i] : 0;
       st += tk[i];
       sp += pages_of(tk[i]);
     }
@@ -415,23 +460,31 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(SchedArgs a) {
       // cumulative tokens and pages only grow, so the admitted set is a prefix
       ok_n += ct <= budget && cp <= free_n;
       if (j == m - 1) sm.pref[m] = cp;
+      sm.seq[j] = tk[i];  // (the moved-sequence list is free again)
     }
-    n_adm = sc.sum(ok_n);  // its barrier also publishes sm.empty / sm.pref
-    // the r-th admitted sequence takes the r-th empty slot
+    n_adm = sc.sum(ok_n);  // its barrier also publishes sm.empty / sm.pref / sm.seq
+    // the j-th admitted entry takes the j-th empty slot: its candidate thread
+    // writes the slot, the slot's owner takes its rows
 #pragma unroll
     for (int i = 0; i < K; ++i) {
-      const int s = tid * K + i, r = erank[i];
-      if (r < 0 || r >= n_adm) continue;
-      const int q = ring((int64_t)head + r, Q);
-      seq[i] = a.queue_seq[q];
-      fin[i] = a.queue_fin[q];
-      ctx[i] = a.queue_tok[q];
-      ord[i] = next_order + r;
-      rows[i] = ctx[i];
-      a.slot_seq[s] = seq[i];
-      a.slot_order[s] = ord[i];
-      a.slot_fin[s] = fin[i];
-      a.context_lens[s] = ctx[i];
+      const int j = tid * K + i;
+      if (j >= n_adm) continue;
+      const int s = sm.empty[j];
+      int id = qid[i], fn = qfn[i];
+      if constexpr (!kPre) {
+        const int q = ring((int64_t)head + j, Q);
+        id = a.queue_seq[q];
+        fn = a.queue_fin[q];
+      }
+      a.slot_seq[s] = id;
+      a.slot_order[s] = next_order + j;
+      a.slot_fin[s] = fn;
+      a.context_lens[s] = sm.seq[j];
+    }
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+      const int r = erank[i];
+      if (r >= 0 && r < n_adm) rows[i] = sm.seq[r];
     }
     // pages: the f-th page popped overall is free_pages[free_n - 1 - f]
     const int total = n_adm > 0 ? sm.pref[n_adm] : 0;
