@@ -28,6 +28,13 @@ constexpr int kDefaultPagesPerSplit = 128;
 #define PA_STREAM_CU_DEN 16
 #endif
 constexpr int kStreamCuNum = PA_STREAM_CU_NUM, kStreamCuDen = PA_STREAM_CU_DEN;
+// share of the CUs the mixed launch gives the prefill chunks
+#ifndef PA_MIXED_PF_NUM
+#define PA_MIXED_PF_NUM 1
+#endif
+#ifndef PA_MIXED_PF_DEN
+#define PA_MIXED_PF_DEN 4
+#endif
 
 struct Plan {
   int s = 0;
@@ -252,7 +259,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
       // grid) for the decode rows: one grid of one workgroup per CU
       // (measured on the mixed Mixtral batch: splits 176..208 / 48..80 of the
       // 256 CUs are within 2 % of 192 / 64)
-      const int g_pf = cus / 4 > 0 ? cus / 4 : 1;
+      const int g_pf = cus * PA_MIXED_PF_NUM / PA_MIXED_PF_DEN > 0 ? cus * PA_MIXED_PF_NUM / PA_MIXED_PF_DEN : 1;
       const int g_dec = G < cus - g_pf ? G : (cus - g_pf > p.g_min ? cus - g_pf : (int)p.g_min);
       e = pa::launch_mixed(p.s, sa, pf, g_dec, g_dec + g_pf, stream, next_events());
     } else {
