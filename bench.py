@@ -365,7 +365,10 @@ def main():
             "timed_region_us_per_step": round(region_us, 2),
             "attention_us_mean": round(float(np.mean(attn_ms)) * 1e3, 2),
             "attention_us_median": round(float(np.median(attn_ms)) * 1e3, 2),
-            "reduce_us_mean": round(float(np.mean(red_ms)) * 1e3, 2),
+            # the split-K path's reduction kernel; the stream-K and mixed
+            # launches merge inside the attention kernel and have none
+            "reduce_us_mean": (round(float(np.mean(red_ms)) * 1e3, 2) if args.pages_per_split > 0
+                               else None),
             "step_us_median": round(float(np.median(step_ms)) * 1e3, 2),
             "kv_gb_per_s_step": round(by["total"] / (float(np.median(step_ms)) / 1e3) / 1e9, 1),
             "algorithmic_bytes": by,
