@@ -1,0 +1,48 @@
+"""Seeded random sweep of the attention calls against the oracle: each case
+draws a shape (KV heads, group size, head dim, dtype), a context mix (empty,
+one-token, page-boundary and long contexts), a launch path (stream-K or an
+explicit split granule) and, for varlen cases, chunk lengths, and runs the
+whole batch through the library and the oracle.  The draws are fixed by the
+case number, so a failing case names a reproducible batch."""
+import numpy as np
+import pytest
+
+from paper_2504_09345_amd import workloads as W
+
+from parity_util import announce, assert_parity, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+EDGE_CTX = [0, 1, 2, 15, 16, 17, 31, 32, 33, 255, 256, 257]
+
+
+def _draw(case):
+    rng = np.random.default_rng(1000 + case)
+    H_kv = int(rng.choice([1, 2, 4, 8]))
+    s = int(rng.choice([1, 2, 4, 6, 8]))
+    D = int(rng.choice([64, 128]))
+    dtype = "bf16" if rng.random() < 0.75 else "fp32"
+    B = int(rng.integers(1, 40))
+    ctx = [int(rng.choice(EDGE_CTX)) if rng.random() < 0.4 else int(rng.integers(1, 3000)) for _ in range(B)]
+    pps = int(rng.choice([0, 0, 0, 1, 7]))
+    varlen = rng.random() < 0.35
+    return H_kv, s, D, dtype, ctx, pps, varlen, rng
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_batch(case):
+    H_kv, s, D, dtype, ctx, pps, varlen, rng = _draw(case)
+    announce(f"random case {case}: H_kv={H_kv} s={s} D={D} {dtype} B={len(ctx)} pps={pps} varlen={varlen}")
+    if not varlen:
+        b = W.generate("tiny", seed=2000 + case, dtype=dtype,
+                       overrides=dict(H_q=s * H_kv, H_kv=H_kv, D=D, ctx=("list", ctx), pool=("factor", 1.3)))
+    else:
+        n_pre = int(rng.integers(1, 4))
+        chunk = int(rng.integers(2, 300))
+        b = W.generate("mixed", seed=2000 + case, dtype=dtype,
+                       overrides=dict(H_q=s * H_kv, H_kv=H_kv, D=D, prefill=(n_pre, chunk, 0, 700),
+                                      decode=(int(rng.integers(0, 20)), 1, 2500), pool=("factor", 1.3)))
+    got = run_gpu(b, pages_per_split=pps)
+    # varlen rows of fp32 or D = 64 chunks take the per-row kernel; the MFMA
+    # prefill rows keep P in two bf16 parts (strict floor only for decode)
+    assert_parity(got, run_oracle(b), strict=not varlen, what=f"case {case}")
