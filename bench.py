@@ -4,7 +4,9 @@
 One step = one paged_attn call (the stream-K attention kernel, which also
 merges the items its ranges cut; for the mixed workload one paged_attn_varlen
 call, whose one kernel runs the decode rows and the prefill chunks side by
-side) over a whole synthetic batch whose inputs are already resident in HBM.
+side; for the prefill-only workload one launch of the chunked-prefill kernel,
+whose roofline is the matrix-core FLOP peak) over a whole synthetic batch
+whose inputs are already resident in HBM.
 Default workload: Mixtral-8x7B-shaped decode, batch 256, 32 query / 8 KV
 heads, head dim 128, bf16 KV, page size 16, context lengths uniform in
 [512, 2048], pages randomly placed in a pool 1.25x the need.
@@ -44,12 +46,14 @@ from paper_2504_09345_amd import binding as pb  # noqa: E402
 from paper_2504_09345_amd import workloads as W  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD public figure
+MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix peak, AMD public figure
 METRIC = "decode attention seqs/sec and achieved KV GB/s (% of MI355X HBM peak)"
 WORKLOAD_NAMES = {
     "mixtral-256": "mixtral-8x7b-decode-b256-ctx512-2048",
     "long-ctx-64": "mixtral-8x7b-decode-b64-ctx8192-32768",
     "dbrx-512": "dbrx-decode-b512-lognormal-ctx128-8192",
     "mixed": "mixtral-8x7b-mixed-8x512prefill-512decode",
+    "prefill-8x512": "mixtral-8x7b-prefill-8x512",
     "tiny": "tiny-decode-b4",
 }
 
@@ -326,6 +330,16 @@ def main():
     achieved = by["total"] / attn_avg_s / 1e9
     value = batch.num_seqs * K / wall
     ms_per_step = wall / K * 1e3
+    # a batch of prefill chunks only is one launch of the chunked-prefill
+    # kernel, bound by the matrix cores: its roofline is FLOP-based
+    prefill_only = qsl is not None and bool((batch.q_lens > 1).all())
+    if prefill_only:
+        tflops = fl / attn_avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(tflops, 1), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / MFMA_PEAK_TFLOPS, 4), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic}
 
     res = {
         "metric": METRIC,
@@ -349,12 +363,7 @@ def main():
             "kv_append": bool(args.append),
         },
         "roofline": {
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic,
+            **roof,
             "traffic_unit": "bytes/launch",
             "traffic_source": traffic_src,
             "timing": ("events around the timed region, per launch" if single_launch

@@ -216,13 +216,19 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
   // a quarter of the CUs would hold the launch up; the kernels then run one
   // after the other, prefill on every CU.
   const int64_t chunk_rows = (int64_t)dims->num_q_rows - dims->num_seqs;
-  const bool mixed = p.stream && p.prefill && dims->num_seqs > 0 &&
+  // Every sequence carrying max_q_len > 1 rows (the rows add up to
+  // num_seqs * max_q_len) leaves no decode row: the stream-K kernel, which
+  // takes only one-row sequences, would find no work and is not launched.
+  const bool no_decode_rows = p.prefill && dims->max_q_len > 1 &&
+                              (int64_t)dims->max_q_len * dims->num_seqs == dims->num_q_rows;
+  const bool launch_stream = p.stream && dims->num_seqs > 0 && !no_decode_rows;
+  const bool mixed = launch_stream && p.prefill &&
                      chunk_rows * p.s <= (int64_t)40 * dims->num_seqs &&
                      pa::mixed_supported(dims->dtype, dims->head_dim, p.s, p.W);
   // attention kernels in launch order: stream-K (or mixed), prefill, split-K;
   // the timing events bracket the first one's start and the last one's end
   // (rows > 0 here, so every planned kernel launches)
-  const int n_attn = (p.stream ? 1 : 0) + (p.prefill && !mixed ? 1 : 0) + (p.split ? 1 : 0);
+  const int n_attn = (launch_stream && !mixed ? 1 : 0) + (p.prefill ? 1 : 0) + (p.split ? 1 : 0);
   int n_launched = 0;
   auto next_events = [&]() {
     pa::KernelEvents k;
@@ -231,7 +237,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     ++n_launched;
     return k;
   };
-  if (p.stream && !mixed && sa.B > 0) {
+  if (launch_stream && !mixed) {
     e = pa::launch_stream(dims->dtype, dims->head_dim, p.s, p.W, sa, G, stream, next_events());
     if (e != hipSuccess) return PA_EHIP;
   }

@@ -15,9 +15,16 @@
 //   S^T[key][row] = K . Q^T   (v_mfma_f32_16x16x32_bf16 per page, K as the A
 //                  operand)
 //   online softmax per row (each lane owns one row and 8 of its keys)
-//   O^T[dim][row] += V^T . P^T (two v_mfma_f32_16x16x32_bf16 over the step's
-//                  keys, one with the bf16 high parts of P and one with the
-//                  low parts: fp32-level accuracy)
+//   O^T[dim][row] += V^T . P^T (one v_mfma_f32_16x16x32_f16 over the step's
+//                  keys: P rounded to fp16, V staged in LDS as fp16)
+// fp16 keeps 11 significant bits against bf16's 8, so P's rounding error is
+// 2^-11 relative (bf16 P alone missed the relative tolerance; fp16 P adds a
+// tenth of what the bf16 rounding of the output costs), and bf16 V converts
+// to fp16 exactly for magnitudes in [2^-17, 2^16).  An item whose V holds a
+// value of 2^16 or more (or inf / NaN), or whose output rows have an RMS
+// below 2^-14 (where fp16's subnormal V could matter), is computed again in
+// a bf16 pass: V as loaded, P as its bf16 high and low parts in two
+// v_mfma_f32_16x16x32_bf16 (fp32-level accuracy).
 // Computing the transposed products keeps "lane l % 16 = query row" in every
 // accumulator, so the softmax statistics, the P operand and the O rescale all
 // stay in the lane that owns the row: no register transposes.

@@ -14,6 +14,10 @@ using mfma::f32x4_t;
 using mfma::lds_s16x4_t;
 using mfma::s16x4_t;
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+template <bool V> struct PfBool { static constexpr bool value = V; };
 
 constexpr int kPfWaves = 8;
 constexpr int kPfThreads = 64 * kPfWaves;
@@ -34,6 +38,7 @@ struct PrefillSmem {
   __attribute__((aligned(16))) uint8_t v[kPfLdsSteps][kPfStep * kPage * mfma::kD * 2];
   int32_t bt[kPfMaxPages];
   int32_t scan[kPfThreads];
+  int32_t vwide;  // the item needs the bf16 pass (V outside the fp16 range, or tiny output rows)
 };
 
 // Prefill workgroup `bid` of a grid of G; s_cum holds B + 1 ints of LDS.
@@ -135,15 +140,12 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
       const int p = m / S, h = m - p * S;
       const bool valid = p < npos;
       lim[rb] = valid ? lim0 + p : -1;
-      mrow[rb] = kMInit;
-      acc_l[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) acc[rb][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       const uint16_t* qrow = qg + ((int64_t)(q0 + pos0 + (valid ? p : 0)) * a.H_q + (int64_t)g * S + h) * D;
 #pragma unroll
       for (int st = 0; st < KSTEPS; ++st)
         qt[rb][st] = valid ? *reinterpret_cast<const u32x4*>(qrow + st * 32 + Gq * 8) : u32x4{0, 0, 0, 0};
     }
+    if (tid == 0) sm.vwide = 0;
     __syncthreads();  // s_bt is filled
 
     // Slots past the context (the tail of the last page) are staged as zeros:
@@ -165,10 +167,27 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
       kr = __builtin_amdgcn_raw_buffer_load_b128(rk, st_ld, 0, kPfLoadPolicy);
       vr = __builtin_amdgcn_raw_buffer_load_b128(rv, st_ld, 0, kPfLoadPolicy);
     };
-    auto stash = [&](int t, const u32x4& kr, const u32x4& vr) {
+    // With F16, V is staged as fp16: bf16 magnitudes in [2^-17, 2^16) and
+    // zeros convert exactly, smaller ones to fp16 subnormals (absolute error
+    // <= 2^-25); a chunk with a larger, infinite or NaN value marks the item,
+    // which is then run again in bf16.
+    auto stash = [&](auto f16, int t, const u32x4& kr, const u32x4& vr) {
       const int buf = t % kPfLdsSteps;
       *reinterpret_cast<u32x4*>(s_k[buf] + st_off) = kr;
-      *reinterpret_cast<u32x4*>(s_v[buf] + st_off_v) = vr;
+      if constexpr (decltype(f16)::value) {
+        u32x4 vh;
+        uint32_t mx = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const f32x2_t f = f32x2_t{__uint_as_float(vr[i] << 16), __uint_as_float(vr[i] & 0xffff0000u)};
+          vh[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2_t));
+          mx = max(mx, max(vr[i] & 0x7fffu, (vr[i] >> 16) & 0x7fffu));
+        }
+        *reinterpret_cast<u32x4*>(s_v[buf] + st_off_v) = vh;
+        if (mx >= 0x4780u) sm.vwide = 1;  // |v| >= 2^16, inf or NaN
+      } else {
+        *reinterpret_cast<u32x4*>(s_v[buf] + st_off_v) = vr;
+      }
     };
     // S^T = K . Q^T for the pages of step t (A: key lane%16, dims 32 st +
     // 8 (lane/16) .. +8), each K read shared by both row blocks
@@ -194,7 +213,10 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
     // acc_l holds its row's sum).
     const bf16x8_t ones = __builtin_bit_cast(
         bf16x8_t, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
-    auto softmax_pv = [&](int t, const f32x4_t (&sc)[kPfBlocks][kPfStep]) {
+    const f16x8_t ones_h = __builtin_bit_cast(
+        f16x8_t, u32x4{0x3c003c00u, 0x3c003c00u, 0x3c003c00u, 0x3c003c00u});
+    auto softmax_pv = [&](auto f16, int t, const f32x4_t (&sc)[kPfBlocks][kPfStep]) {
+      constexpr bool F16 = decltype(f16)::value;
       const uint8_t* vt = s_v[t % kPfLdsSteps];
       const int key0 = t * kPfStep * kPage;  // first key of the step
       // this lane holds keys key0 + 16 pp + 4 (lane/16) + i of its row; the
@@ -250,36 +272,63 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
         }
         weights();
       }
-      // P operands: k slots 8 (lane/16) + 4 pp + i hold key 4 (lane/16) + i of page pp
-      bf16x8_t phi[kPfBlocks], plo[kPfBlocks];
-#pragma unroll
-      for (int rb = 0; rb < kPfBlocks; ++rb) {
-        s16x4_t h[kPfStep], l[kPfStep];
-#pragma unroll
-        for (int pp = 0; pp < kPfStep; ++pp) {
-          const float q4[4] = {pw[rb][pp * 4], pw[rb][pp * 4 + 1], pw[rb][pp * 4 + 2], pw[rb][pp * 4 + 3]};
-          mfma::split_hi_lo(q4, h[pp], l[pp]);
-        }
-        phi[rb] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
-        plo[rb] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(l[0], l[1], 0, 1, 2, 3, 4, 5, 6, 7));
-        acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, phi[rb], acc_l[rb], 0, 0, 0);
-        acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, plo[rb], acc_l[rb], 0, 0, 0);
-      }
-      // lane p of group Gq addresses key 4 Gq + p / 4, dims 16 mb + 4 (p % 4)
-      // of each page; the two transposed reads form the A operand's k slots in
-      // the same page-major order as P
+      // P operands: k slots 8 (lane/16) + 4 pp + i hold key 4 (lane/16) + i
+      // of page pp, i.e. the lane's 8 weights in order.  V^T: lane p of group
+      // Gq addresses key 4 Gq + p / 4, dims 16 mb + 4 (p % 4) of each page;
+      // the two transposed reads form the A operand's k slots in the same
+      // page-major order as P.
       const int vkey = 4 * Gq + (n >> 2);
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const int d = mb * 16 + 4 * (n & 3);
-        const int off = mfma::swz_v(vkey, d >> 3) + (d & 7) * 2;
-        const s16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + off));
-        const s16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + KT + off));
-        const bf16x8_t va = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+      if constexpr (F16) {
+        // fp16 P (nearest even, relative error <= 2^-11) and fp16 V: one product
+        f16x8_t ph[kPfBlocks];
 #pragma unroll
         for (int rb = 0; rb < kPfBlocks; ++rb) {
-          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[rb], acc[rb][mb], 0, 0, 0);
-          acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[rb], acc[rb][mb], 0, 0, 0);
+          u32x4 w4;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            w4[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{pw[rb][2 * i], pw[rb][2 * i + 1]}), f16x2_t));
+          ph[rb] = __builtin_bit_cast(f16x8_t, w4);
+          acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ones_h, ph[rb], acc_l[rb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int d = mb * 16 + 4 * (n & 3);
+          const int off = mfma::swz_v(vkey, d >> 3) + (d & 7) * 2;
+          const s16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + off));
+          const s16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + KT + off));
+          const f16x8_t va = __builtin_bit_cast(f16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+          for (int rb = 0; rb < kPfBlocks; ++rb)
+            acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, ph[rb], acc[rb][mb], 0, 0, 0);
+        }
+      } else {
+        // bf16 V and P's bf16 high and low parts: two products
+        bf16x8_t phi[kPfBlocks], plo[kPfBlocks];
+#pragma unroll
+        for (int rb = 0; rb < kPfBlocks; ++rb) {
+          s16x4_t h[kPfStep], l[kPfStep];
+#pragma unroll
+          for (int pp = 0; pp < kPfStep; ++pp) {
+            const float q4[4] = {pw[rb][pp * 4], pw[rb][pp * 4 + 1], pw[rb][pp * 4 + 2], pw[rb][pp * 4 + 3]};
+            mfma::split_hi_lo(q4, h[pp], l[pp]);
+          }
+          phi[rb] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+          plo[rb] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(l[0], l[1], 0, 1, 2, 3, 4, 5, 6, 7));
+          acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, phi[rb], acc_l[rb], 0, 0, 0);
+          acc_l[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, plo[rb], acc_l[rb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int d = mb * 16 + 4 * (n & 3);
+          const int off = mfma::swz_v(vkey, d >> 3) + (d & 7) * 2;
+          const s16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + off));
+          const s16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vt + KT + off));
+          const bf16x8_t va = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+          for (int rb = 0; rb < kPfBlocks; ++rb) {
+            acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[rb], acc[rb][mb], 0, 0, 0);
+            acc[rb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[rb], acc[rb][mb], 0, 0, 0);
+          }
         }
       }
     };
@@ -298,35 +347,75 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
         __syncthreads();
       }
     };
-    u32x4 ka, va, kb, vb;
-    // (scheduling barriers keep the issue order the loop's waits assume)
-    fetch(0, ka, va);
-    __builtin_amdgcn_sched_barrier(0);
-    fetch(1, kb, vb);
-    __builtin_amdgcn_sched_barrier(0);
-    stash(0, ka, va);
-    __builtin_amdgcn_sched_barrier(0);
-    fetch(2, ka, va);
-    __builtin_amdgcn_sched_barrier(0);
-    stash(1, kb, vb);
-    __builtin_amdgcn_sched_barrier(0);
-    fetch(3, kb, vb);
-    __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();  // steps 0 and 1 are in LDS
-    f32x4_t sc[kPfBlocks][kPfStep], sn[kPfBlocks][kPfStep];
-    qk(0, sc);
-    // two steps per trip; with nst odd the last trip's second step is null
-    for (int t = 0; t < nst; t += 2) {
-      step_barrier(t);
-      stash(t + 2, ka, va);
-      fetch(t + 4, ka, va);
-      qk(t + 1, sn);
-      softmax_pv(t, sc);
-      step_barrier(t + 1);
-      stash(t + 3, kb, vb);
-      fetch(t + 5, kb, vb);
-      qk(t + 2, sc);
-      softmax_pv(t + 1, sn);
+    // One pass over the item's steps; acc, acc_l and mrow start afresh.
+    auto pipeline = [&](auto f16) {
+#pragma unroll
+      for (int rb = 0; rb < kPfBlocks; ++rb) {
+        mrow[rb] = kMInit;
+        acc_l[rb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) acc[rb][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
+      u32x4 ka, va, kb, vb;
+      // (scheduling barriers keep the issue order the loop's waits assume)
+      fetch(0, ka, va);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(1, kb, vb);
+      __builtin_amdgcn_sched_barrier(0);
+      stash(f16, 0, ka, va);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(2, ka, va);
+      __builtin_amdgcn_sched_barrier(0);
+      stash(f16, 1, kb, vb);
+      __builtin_amdgcn_sched_barrier(0);
+      fetch(3, kb, vb);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();  // steps 0 and 1 are in LDS
+      f32x4_t sc[kPfBlocks][kPfStep], sn[kPfBlocks][kPfStep];
+      qk(0, sc);
+      // two steps per trip; with nst odd the last trip's second step is null
+      for (int t = 0; t < nst; t += 2) {
+        step_barrier(t);
+        stash(f16, t + 2, ka, va);
+        fetch(t + 4, ka, va);
+        qk(t + 1, sn);
+        softmax_pv(f16, t, sc);
+        step_barrier(t + 1);
+        stash(f16, t + 3, kb, vb);
+        fetch(t + 5, kb, vb);
+        qk(t + 2, sc);
+        softmax_pv(f16, t + 1, sn);
+      }
+      if constexpr (decltype(f16)::value) {
+        // fp16 V is exact for bf16 magnitudes in [2^-17, 2^16); smaller ones
+        // carry an absolute error <= 2^-25, which stays below a tenth of the
+        // relative tolerance only for rows whose output RMS is >= 2^-14
+        bool tiny = false;
+#pragma unroll
+        for (int rb = 0; rb < kPfBlocks; ++rb) {
+          const float inv = 1.0f / acc_l[rb][0];
+          float ss = 0.0f;
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ss = fmaf(acc[rb][mb][i] * inv, acc[rb][mb][i] * inv, ss);
+          // ss of the row's D dims (a NaN row is left as it is)
+          const float row_ss = rows4_sum(ss);
+          tiny |= lim[rb] >= 0 && row_ss < (float)D * 0x1p-28f;
+        }
+        if (__builtin_amdgcn_ballot_w64(tiny) != 0 && lane == 0) sm.vwide = 1;
+      }
+    };
+    // fp16 pass; an item whose V does not fit fp16 (or whose output rows are
+    // too small for fp16's subnormal V) is recomputed in bf16
+    pipeline(PfBool<true>{});
+    __syncthreads();  // every stash of the pass has set or left the flag
+    if (sm.vwide) {
+      if (npg > kPfMaxPages) {  // the pass slid the block-table window: back to page 0
+        for (int i = tid; i < kPfMaxPages; i += kPfThreads) s_bt[i] = bt.page(b, i);
+        __syncthreads();
+      }
+      pipeline(PfBool<false>{});
     }
 
     // normalise and store straight from the accumulators: lane (n, Gq) holds

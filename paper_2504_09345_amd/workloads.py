@@ -53,6 +53,9 @@ CONFIGS = {
     # decode sequences, in one launch
     "mixed": dict(kind="varlen", H_q=32, H_kv=8, D=128, prefill=(8, 512, 0, 1536),
                   decode=(512, 256, 4096), pool=("factor", 1.25), std=0.5),
+    # the same 8 prefill chunks on their own (the chunked-prefill kernel alone)
+    "prefill-8x512": dict(kind="varlen", H_q=32, H_kv=8, D=128, prefill=(8, 512, 0, 1536),
+                          decode=(0, 256, 4096), pool=("factor", 1.25), std=0.5),
 }
 
 

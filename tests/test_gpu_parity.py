@@ -290,12 +290,80 @@ def test_prefill_heavy_batch_runs_kernels_in_turn():
     assert_parity(run_gpu(b), run_oracle(b), strict=False, what="prefill-heavy")
 
 
+@pytest.mark.parametrize("lens", [(64, 64, 64, 64, 64), (64, 40, 64, 2, 64)])
+def test_prefill_only_batches(lens):
+    """Chunks and no decode row.  Equal chunk lengths (the rows add up to
+    num_seqs x max_q_len) let the host skip the stream-K launch; unequal ones
+    launch it and it finds no work.  Both match the oracle."""
+    announce(f"prefill-only batch {lens}")
+    priors = [0, 700, 33, 1500, 16]
+    b = _chunk_batch(4, 85, list(zip(lens, priors)), decode_ctx=[], H_kv=8)
+    assert (b.q_lens > 1).all()
+    assert_parity(run_gpu(b), run_oracle(b), strict=False, what=f"prefill-only {lens}")
+
+
 def test_prefill_poisoned_pool():
     announce("prefill poison")
     b = _chunk_batch(4, 40, [(48, 7), (96, 300), (31, 0)], decode_ctx=[33, 500], poison=True)
     got = run_gpu(b)
     assert np.isfinite(got).all()
     assert_parity(got, run_oracle(b), strict=False)
+
+
+def _scale_v(b, seqs, factor):
+    """V pages of sequences `seqs` times a power of two (exact in bf16)."""
+    v = W.bf16_bits_to_f32(b.v_pages).copy()
+    for j in seqs:
+        v[b.block_table[j, :(int(b.context_lens[j]) + 15) // 16]] *= np.float32(factor)
+    return W.Batch(**{**b.__dict__, "v_pages": W.f32_to_bf16_bits(v)})
+
+
+@pytest.mark.parametrize("H_kv", [2, 8])
+@pytest.mark.parametrize("log2_factor", [17, 40, -6, -12, -24, -60])
+def test_prefill_value_range(H_kv, log2_factor):
+    """Chunk rows whose V is far from unit scale.  Magnitudes of 2^16 and up
+    do not fit fp16, and V below 2^-17 is not exact in it; either way the
+    chunk must still match the oracle in relative terms (the absolute bound
+    is meaningless for scaled values), and the other rows of the batch must
+    stay within the full tolerance.  H_kv = 8 runs the chunks in the mixed
+    decode + prefill launch."""
+    announce(f"prefill V range 2^{log2_factor} H_kv={H_kv}")
+    chunks = [(96, 40), (130, 300), (64, 0), (33, 700)]
+    decode_ctx = [1, 16, 300, 2000] + ([700] * 60 if H_kv == 8 else [])
+    b = _chunk_batch(4, 90 + log2_factor % 17, chunks, decode_ctx=decode_ctx, H_kv=H_kv)
+    chunk_seqs = [j for j in range(b.num_seqs) if b.q_lens[j] > 1]
+    scaled = chunk_seqs[::2]  # every other chunk sequence
+    b = _scale_v(b, scaled, 2.0 ** log2_factor)
+    _assert_scaled_parity(b, scaled, f"2^{log2_factor}")
+
+
+@pytest.mark.parametrize("log2_factor", [0, 17])
+def test_prefill_past_the_block_table_window(log2_factor):
+    """A chunk on 40,000 cached tokens (2,505 pages): the workgroup's window of
+    2,048 block-table entries slides during the item; with V past the fp16
+    range the item's bf16 pass starts again from the first window."""
+    announce(f"prefill 40k context, V x 2^{log2_factor}")
+    b = _chunk_batch(4, 95, [(64, 40000), (40, 100)], decode_ctx=[3, 500])
+    long_seq = [j for j in range(b.num_seqs) if b.context_lens[j] > 40000]
+    assert len(long_seq) == 1 and (int(b.context_lens[long_seq[0]]) + 15) // 16 > 2048
+    scaled = long_seq if log2_factor else []
+    if scaled:
+        b = _scale_v(b, scaled, 2.0 ** log2_factor)
+    _assert_scaled_parity(b, scaled, f"40k context, 2^{log2_factor}")
+
+
+def _assert_scaled_parity(b, scaled, what):
+    """Rows of the `scaled` sequences: relative bound only; the rest: the
+    full tolerance."""
+    got, ref = run_gpu(b), run_oracle(b)
+    qsl = b.query_start_loc
+    rows = np.zeros(got.shape[0], bool)
+    for j in scaled:
+        rows[qsl[j]:qsl[j + 1]] = True
+    if rows.any():
+        st = parity_stats(got[rows], ref[rows])
+        assert st["finite"] and st["max_rel"] <= 5e-3, (what, st)
+    assert_parity(got[~rows], ref[~rows], strict=False, what=f"unscaled rows, {what}")
 
 
 def test_prefill_determinism_and_single_rows_match_decode():

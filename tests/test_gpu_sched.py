@@ -193,5 +193,10 @@ def test_scheduler_feeds_append_and_attention():
         torch.cuda.synchronize()
         assert np.array_equal(dk.cpu().view(torch.int16).numpy().view(np.uint16), k_pool)
         assert np.array_equal(dv.cpu().view(torch.int16).numpy().view(np.uint16), v_pool)
-        assert_parity(out.float().cpu().numpy(), ref, what=f"pass {i}")
+        # decode rows to the strict floor; chunk rows (fp16 P and V on the
+        # matrix cores) to the relative bound, like every chunk test
+        got, qlen = out.float().cpu().numpy(), np.diff(eq)
+        dec = np.repeat(qlen == 1, qlen)
+        assert_parity(got[dec], ref[dec], what=f"pass {i}, decode rows")
+        assert_parity(got[~dec], ref[~dec], strict=False, what=f"pass {i}, chunk rows")
     assert preempted > 0

@@ -37,7 +37,7 @@ def test_tiny_matches_its_description():
     assert used.min() >= 0 and used.max() < 64
 
 
-@pytest.mark.parametrize("name", ["mixtral-256", "long-ctx-64", "dbrx-512", "mixed"])
+@pytest.mark.parametrize("name", ["mixtral-256", "long-ctx-64", "dbrx-512", "mixed", "prefill-8x512"])
 def test_length_mixes(name):
     # only the small draws: lengths and the page permutation (patch the bulk draw)
     orig = W._fill_normal
@@ -60,6 +60,9 @@ def test_length_mixes(name):
         assert (ql[:8] == 512).all() and (ql[8:] == 1).all() and len(ql) == 520
         assert (ctx[:8] >= 512).all() and (ctx[:8] <= 2048).all()
         assert (ctx[8:] >= 256).all() and (ctx[8:] <= 4096).all()
+    if name == "prefill-8x512":
+        assert (b.q_lens == 512).all() and len(ctx) == 8
+        assert (ctx >= 512).all() and (ctx <= 2048).all()
     need = int(((ctx + 15) // 16).sum())
     assert b.meta["pages_used"] == need
     # pool sized 1.25x the need, pages disjoint
