@@ -191,8 +191,18 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
     };
     // S^T = K . Q^T for the pages of step t (A: key lane%16, dims 32 st +
     // 8 (lane/16) .. +8), each K read shared by both row blocks
-    auto qk = [&](int t, f32x4_t (&sc)[kPfBlocks][kPfStep]) {
+    // (the step's K operands are read from LDS first, all at once, so their
+    // latency overlaps the staging work issued before the products)
+    typedef u32x4 KOps[kPfStep][KSTEPS];
+    auto k_read = [&](int t, KOps& kv) {
       const uint8_t* kt = s_k[t % kPfLdsSteps];
+#pragma unroll
+      for (int pp = 0; pp < kPfStep; ++pp)
+#pragma unroll
+        for (int st = 0; st < KSTEPS; ++st)
+          kv[pp][st] = *reinterpret_cast<const u32x4*>(kt + pp * KT + mfma::swz(n, st * 4 + Gq));
+    };
+    auto qk = [&](const KOps& kv, f32x4_t (&sc)[kPfBlocks][kPfStep]) {
 #pragma unroll
       for (int rb = 0; rb < kPfBlocks; ++rb)
 #pragma unroll
@@ -200,13 +210,11 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
 #pragma unroll
       for (int pp = 0; pp < kPfStep; ++pp)
 #pragma unroll
-        for (int st = 0; st < KSTEPS; ++st) {
-          const u32x4 kv = *reinterpret_cast<const u32x4*>(kt + pp * KT + mfma::swz(n, st * 4 + Gq));
+        for (int st = 0; st < KSTEPS; ++st)
 #pragma unroll
           for (int rb = 0; rb < kPfBlocks; ++rb)
             sc[rb][pp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, kv), __builtin_bit_cast(bf16x8_t, qt[rb][st]), sc[rb][pp], 0, 0, 0);
-        }
+                __builtin_bit_cast(bf16x8_t, kv[pp][st]), __builtin_bit_cast(bf16x8_t, qt[rb][st]), sc[rb][pp], 0, 0, 0);
     };
     // online softmax of step t's scores and O^T += V^T . P^T.  Row sums come
     // from the matrix cores too: acc_l += ones . P^T (every entry of a lane's
@@ -372,18 +380,24 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
       __builtin_amdgcn_sched_barrier(0);
       __syncthreads();  // steps 0 and 1 are in LDS
       f32x4_t sc[kPfBlocks][kPfStep], sn[kPfBlocks][kPfStep];
-      qk(0, sc);
+      KOps kv;
+      k_read(0, kv);
+      qk(kv, sc);
       // two steps per trip; with nst odd the last trip's second step is null
       for (int t = 0; t < nst; t += 2) {
         step_barrier(t);
+        k_read(t + 1, kv);
+        __builtin_amdgcn_sched_barrier(0);
         stash(f16, t + 2, ka, va);
         fetch(t + 4, ka, va);
-        qk(t + 1, sn);
+        qk(kv, sn);
         softmax_pv(f16, t, sc);
         step_barrier(t + 1);
+        k_read(t + 2, kv);
+        __builtin_amdgcn_sched_barrier(0);
         stash(f16, t + 3, kb, vb);
         fetch(t + 5, kb, vb);
-        qk(t + 2, sc);
+        qk(kv, sc);
         softmax_pv(f16, t + 1, sn);
       }
       if constexpr (decltype(f16)::value) {
