@@ -175,9 +175,25 @@ def _cpu_baseline(batch: W.Batch, target_s: float, max_seqs: int | None):
     reps = max(1, min(200, int(target_s / max(dt, 1e-3))))
     times = [dt] + [run(n) for _ in range(reps - 1)]
     t = float(np.median(times))
-    return dict(value=n / t, unit="seqs/s", cores=oracle.get_threads(), kind="oracle",
-                sample=f"first {n} of {B} sequences of the same batch, {len(times)} runs, "
-                       f"median {t:.3f} s per run (fp32 oracle, OpenMP over rows x heads)")
+    res = dict(value=n / t, unit="seqs/s", cores=oracle.get_threads(), kind="oracle",
+               sample=f"first {n} of {B} sequences of the same batch, {len(times)} runs, "
+                      f"median {t:.3f} s per run (fp32 oracle, OpenMP over rows x heads)")
+    # the same sample's algorithmic bytes per second, and one thread's rate
+    # (a sample of about a tenth of the time budget)
+    q, bt, cl, qsl = sub(n)
+    sub_batch = W.Batch(**{**batch.__dict__, "q": q, "block_table": bt, "context_lens": cl,
+                           "query_start_loc": qsl})
+    res["gb_per_s"] = round(algorithmic_bytes(sub_batch)["total"] / t / 1e9, 2)
+    threads = oracle.get_threads()
+    oracle.set_threads(1)
+    try:
+        n1 = max(1, min(n, int(n * (target_s / 10) / max(dt * threads, 1e-3))))
+        t1 = float(np.median([run(n1) for _ in range(3)]))
+    finally:
+        oracle.set_threads(threads)
+    res["value_1thread"] = n1 / t1
+    res["sample_1thread"] = f"first {n1} sequences, median of 3 runs, {t1:.3f} s per run"
+    return res
 
 
 def main():
@@ -374,6 +390,8 @@ def main():
             "timed_region_us_per_step": round(region_us, 2),
             "attention_us_mean": round(float(np.mean(attn_ms)) * 1e3, 2),
             "attention_us_median": round(float(np.median(attn_ms)) * 1e3, 2),
+            "attention_us_p10": round(float(np.percentile(attn_ms, 10)) * 1e3, 2),
+            "attention_us_p90": round(float(np.percentile(attn_ms, 90)) * 1e3, 2),
             # the split-K path's reduction kernel; the stream-K and mixed
             # launches merge inside the attention kernel and have none
             "reduce_us_mean": (round(float(np.mean(red_ms)) * 1e3, 2) if args.pages_per_split > 0

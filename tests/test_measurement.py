@@ -91,3 +91,14 @@ def test_traffic_is_reported_only_for_the_measured_kernel(tmp_path, monkeypatch)
     assert t2 is None and "stale" in src2
     # no counters for a workload: nothing reported
     assert bench.measured_traffic("tiny") == (None, None)
+
+
+def test_cpu_baseline_reports_all_cores_one_thread_and_bytes():
+    """The oracle leg on a small batch: rates with every thread and with one,
+    and the sample's algorithmic bytes per second."""
+    b = W.generate("tiny", seed=0)
+    r = bench._cpu_baseline(b, 0.3, None)
+    assert r["kind"] == "oracle" and r["unit"] == "seqs/s"
+    assert r["value"] > 0 and r["value_1thread"] > 0 and r["cores"] >= 1
+    full = bench.algorithmic_bytes(b)["total"]
+    assert 0 < r["gb_per_s"] <= full * r["value"] / b.num_seqs / 1e9 * 1.01 + 1e-6
