@@ -183,7 +183,7 @@ def _cpu_baseline(batch: W.Batch, target_s: float, max_seqs: int | None):
     q, bt, cl, qsl = sub(n)
     sub_batch = W.Batch(**{**batch.__dict__, "q": q, "block_table": bt, "context_lens": cl,
                            "query_start_loc": qsl})
-    res["gb_per_s"] = round(algorithmic_bytes(sub_batch)["total"] / t / 1e9, 2)
+    res["gb_per_s"] = float(f"{algorithmic_bytes(sub_batch)['total'] / t / 1e9:.4g}")
     threads = oracle.get_threads()
     oracle.set_threads(1)
     try:
