@@ -145,7 +145,12 @@ int paged_attn(const void *q, const void *k_pages, const void *v_pages,
 
 /* Mixed batch: causal prefill chunks and decode rows in one call.  Decode
  * rows take the stream-K kernel; chunk rows (L_b > 1) take an MFMA kernel
- * (bf16, head_dim 128) or, otherwise, the per-row split-K kernel.
+ * (bf16, head_dim 128) or, otherwise, the per-row split-K kernel.  The MFMA
+ * kernel forms P.V with P rounded to fp16 (relative error 2^-11) and V in
+ * fp16 (exact for bf16 magnitudes in [2^-17, 2^16)); a chunk block whose V
+ * leaves that range (or holds inf / NaN), or whose output rows have an RMS
+ * below 2^-14, is computed again with fp32-level P.V.  When every sequence
+ * has max_q_len > 1 rows, only the chunk kernel runs.
  * Same as paged_attn, with q/out of [num_q_rows][H_q][D] and the device array
  * query_start_loc (see layouts).  Row j of a chunk of length L in a sequence
  * of context C attends to positions 0 .. C - L + j.  dims->num_q_rows must

@@ -44,5 +44,5 @@ def test_random_batch(case):
                                       decode=(int(rng.integers(0, 20)), 1, 2500), pool=("factor", 1.3)))
     got = run_gpu(b, pages_per_split=pps)
     # varlen rows of fp32 or D = 64 chunks take the per-row kernel; the MFMA
-    # prefill rows keep P in two bf16 parts (strict floor only for decode)
+    # prefill rows round P and V to fp16 (the strict floor is for decode only)
     assert_parity(got, run_oracle(b), strict=not varlen, what=f"case {case}")
