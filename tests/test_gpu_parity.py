@@ -337,6 +337,41 @@ def test_prefill_value_range(H_kv, log2_factor):
     _assert_scaled_parity(b, scaled, f"2^{log2_factor}")
 
 
+@pytest.mark.parametrize("value", ["nan", "inf"])
+def test_prefill_nonfinite_v(value):
+    """A NaN or infinity in one V element that chunk rows attend to: the item
+    takes the bf16 pass; the rows that see that key are non-finite exactly
+    where the oracle's are, and every row outside the key's work item
+    matches the oracle.  Rows of that item before the key are left open:
+    their zero weight meets the value inside the matrix product (0 x inf is
+    NaN), where the oracle never visits a masked key."""
+    announce(f"prefill V {value}")
+    b = _chunk_batch(4, 88, [(96, 40), (130, 300), (64, 0)], decode_ctx=[16, 300], H_kv=8)
+    seqs = [j for j in range(b.num_seqs) if b.q_lens[j] > 1]
+    j = seqs[1]
+    C, L = int(b.context_lens[j]), int(b.q_lens[j])
+    r_key = 20
+    t = C - L + r_key  # key of chunk row 20: rows 20.. see it
+    v = b.v_pages.copy()
+    v[b.block_table[j, t // 16], 1, t % 16, 5] = W.BF16_NAN if value == "nan" else np.uint16(0x7F80)
+    b = W.Batch(**{**b.__dict__, "v_pages": v})
+    got, ref = run_gpu(b), run_oracle(b)
+    q0 = int(b.query_start_loc[j])
+    # rows before the key in its work item (64 positions at s = 4), which
+    # runs the key's step for all of its rows
+    open_rows = np.zeros(got.shape[0], bool)
+    open_rows[q0:q0 + r_key] = True
+    sees = np.zeros(got.shape[0], bool)
+    sees[q0 + r_key:q0 + L] = True
+    assert (~np.isfinite(ref[sees])).any()
+    assert np.array_equal(~np.isfinite(got[sees]), ~np.isfinite(ref[sees]))
+    fin = np.isfinite(ref[sees])
+    st = parity_stats(np.where(fin, got[sees], 0), np.where(fin, ref[sees], 0))
+    assert st["max_abs"] <= 1e-2 and st["max_rel"] <= 5e-3, st
+    rest = ~(sees | open_rows)
+    assert_parity(got[rest], ref[rest], strict=False, what=f"rows away from the {value}")
+
+
 @pytest.mark.parametrize("log2_factor", [0, 17])
 def test_prefill_past_the_block_table_window(log2_factor):
     """A chunk on 40,000 cached tokens (2,505 pages): the workgroup's window of
