@@ -372,13 +372,16 @@ def test_prefill_nonfinite_v(value):
     assert_parity(got[rest], ref[rest], strict=False, what=f"rows away from the {value}")
 
 
+@pytest.mark.parametrize("H_kv", [2, 8])
 @pytest.mark.parametrize("log2_factor", [0, 17])
-def test_prefill_past_the_block_table_window(log2_factor):
+def test_prefill_past_the_block_table_window(log2_factor, H_kv):
     """A chunk on 40,000 cached tokens (2,505 pages): the workgroup's window of
     2,048 block-table entries slides during the item; with V past the fp16
-    range the item's bf16 pass starts again from the first window."""
-    announce(f"prefill 40k context, V x 2^{log2_factor}")
-    b = _chunk_batch(4, 95, [(64, 40000), (40, 100)], decode_ctx=[3, 500])
+    range the item's bf16 pass starts again from the first window.  H_kv = 8
+    with ten decode rows runs the chunks in the mixed launch."""
+    announce(f"prefill 40k context, V x 2^{log2_factor}, H_kv={H_kv}")
+    decode_ctx = [3, 500] + ([16, 900, 33, 64, 200, 1000, 7, 300] if H_kv == 8 else [])
+    b = _chunk_batch(4, 95, [(64, 40000), (40, 100)], decode_ctx=decode_ctx, H_kv=H_kv)
     long_seq = [j for j in range(b.num_seqs) if b.context_lens[j] > 40000]
     assert len(long_seq) == 1 and (int(b.context_lens[long_seq[0]]) + 15) // 16 > 2048
     scaled = long_seq if log2_factor else []
