@@ -134,9 +134,11 @@ def measured_traffic(workload: str):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary (FETCH_SIZE and WRITE_SIZE passes, scaled by a known-size copy),
     or None when there is none or the kernel sources changed since."""
-    path = os.path.join(ROOT, "profiles", f"stream_kernel_{workload}_pmc.json")
-    if not os.path.exists(path):
+    import glob
+    found = sorted(glob.glob(os.path.join(ROOT, "profiles", f"*_{workload}_pmc.json")))
+    if not found:
         return None, None
+    path = found[0]
     rec = json.load(open(path))
     h = hashlib.sha256()
     for f in rec["source_files"]:
