@@ -31,6 +31,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import glob
 import hashlib
 import json
 import os
@@ -134,7 +135,6 @@ def measured_traffic(workload: str):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary (FETCH_SIZE and WRITE_SIZE passes, scaled by a known-size copy),
     or None when there is none or the kernel sources changed since."""
-    import glob
     found = sorted(glob.glob(os.path.join(ROOT, "profiles", f"*_{workload}_pmc.json")))
     if not found:
         return None, None
