@@ -412,26 +412,28 @@ def main():
         res["overlap_gemm"] = _overlap_gemm(torch, batch, dev_q, k0, v0, bt, cl, batch.scale,
                                             max(5, min(K, 20)), args.workload)
     if args.sched:
-        res["scheduler"] = _sched_bench(torch, batch, K, args.seed, not args.no_cpu_baseline)
+        res["scheduler"], sched_replay = _sched_bench(torch, batch, K, args.seed)
     if args.perf_model:
         res["perf_model"] = _perf_model_leg(torch, achieved * 1e9)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = _cpu_baseline(batch, args.cpu_baseline_seconds, None)
         res["cpu_baseline"]["host_cpu"] = _cpu_model()
+        if args.sched:
+            res["cpu_baseline"]["scheduler"] = _cpu_sched_baseline(sched_replay)
     print(json.dumps(res))
     return 0
 
 
 # scheduler step measurement.
-def _sched_bench(torch, batch, steps, seed, with_cpu):
+def _sched_bench(torch, batch, steps, seed):
     """Steady-state scheduler steps for this batch's shape: one slot per
     sequence, the batch's page pool, block-table rows long enough for its
     longest context, and an arrival stream of the MTBench-like mix (Table 4,
     generation up to 256) at a rate that keeps every slot busy and the queue
     non-empty.  The arrivals of every step are resident in HBM before timing.
     Returns the per-step kernel time (HIP events around each launch), the
-    wall-clock steps/s of back-to-back steps, the step's counts, and the
-    oracle's CPU time per step on the same stream as a reported baseline."""
+    wall-clock steps/s of back-to-back steps and the step's counts, plus what
+    the CPU-baseline leg needs to replay the same stream on the oracle."""
     S = batch.num_seqs
     P = int(batch.k_pages.shape[0])
     MP = max(int(batch.block_table.shape[1]), (450 + 256 + 15) // 16)
@@ -484,18 +486,24 @@ def _sched_bench(torch, batch, steps, seed, with_cpu):
            "mean_decode_slots": round(float(inf[:, 4].mean()), 1),
            "admitted": int(inf[:, 3].sum()), "finished": int(inf[:, 1].sum()),
            "preempted": int(inf[:, 2].sum()), "rejected_steps": int((inf[:, 0] < 0).sum())}
-    if with_cpu:
-        import oracle
-        ost = oracle.sched_init(S, P, MP, Q)
-        for ids, pr, fn in stream_in[:warm]:
-            ost, *_ = oracle.schedule_step(ost, n_real, ids, pr, fn)
-        t0 = time.perf_counter()
-        for ids, pr, fn in stream_in[warm:warm + steps]:
-            ost, *_ = oracle.schedule_step(ost, n_real, ids, pr, fn)
-        res["cpu_oracle_us_per_step"] = round((time.perf_counter() - t0) / steps * 1e6, 2)
-        res["cpu_oracle_note"] = ("oracle step incl. its Python marshalling (copies of the state "
-                                  "arrays), one thread")
-    return res
+    # what the CPU-baseline leg needs to replay the same stream on the oracle
+    replay = dict(S=S, P=P, MP=MP, Q=Q, n_real=n_real, warm=warm, steps=steps, stream_in=stream_in)
+    return res, replay
+
+
+def _cpu_sched_baseline(replay):
+    """The oracle's scheduler step on the same arrival stream (part of the CPU
+    baseline): mean time per step after the same warm-up."""
+    import oracle
+    r = replay
+    ost = oracle.sched_init(r["S"], r["P"], r["MP"], r["Q"])
+    for ids, pr, fn in r["stream_in"][:r["warm"]]:
+        ost, *_ = oracle.schedule_step(ost, r["n_real"], ids, pr, fn)
+    t0 = time.perf_counter()
+    for ids, pr, fn in r["stream_in"][r["warm"]:r["warm"] + r["steps"]]:
+        ost, *_ = oracle.schedule_step(ost, r["n_real"], ids, pr, fn)
+    return {"us_per_step": round((time.perf_counter() - t0) / r["steps"] * 1e6, 2), "unit": "us/step",
+            "note": "oracle step incl. its Python marshalling (copies of the state arrays), one thread"}
 
 
 # performance model for an MI355X-hosted KV cache.
