@@ -5,9 +5,12 @@ sub-batches for sampled checks, and the tolerance rule.
 Tolerance (bf16 inputs, fp32 accumulation): max abs error 1e-2 and max rel
 error 5e-3.  Relative error is taken against max(|ref|, rho) with rho the
 RMS of that (row, head) reference vector, so that entries near zero do not
-divide by ~0; the decode path, which keeps P in fp32, must also pass with the
-fixed floor max(|ref|, 1e-3).  A bf16 output alone contributes at most
-2^-9 = 1.95e-3 relative error (round to nearest).
+divide by ~0.  The decode tests also check the fixed floor max(|ref|, 1e-3)
+(decode keeps P in fp32, or as bf16 high + low parts of ~16 significant bits
+on the matrix cores).  A bf16 output alone contributes up to 2^-8 = 3.9e-3
+relative error (8 significant bits, round to nearest), so that floor leaves
+little room for entries near 1e-3 and is a check of the committed cases
+rather than a bound.
 """
 from __future__ import annotations
 
