@@ -223,6 +223,8 @@ def main():
                          "measured host-to-device copy rate (adds a perf_model object)")
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hbm-probe", action="store_true",
+                    help="also time plain device reads and copies of multi-GB buffers (context only)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB before timing "
                          "(a known-size kernel for scaling profiler byte counters)")
@@ -413,6 +415,8 @@ def main():
                                             max(5, min(K, 20)), args.workload)
     if args.sched:
         res["scheduler"], sched_replay = _sched_bench(torch, batch, K, args.seed)
+    if args.hbm_probe:
+        res["hbm_probe"] = _hbm_probe(torch)
     if args.perf_model:
         res["perf_model"] = _perf_model_leg(torch, achieved * 1e9)
     if not args.no_cpu_baseline:
@@ -489,6 +493,34 @@ def _sched_bench(torch, batch, steps, seed):
     # what the CPU-baseline leg needs to replay the same stream on the oracle
     replay = dict(S=S, P=P, MP=MP, Q=Q, n_real=n_real, warm=warm, steps=steps, stream_in=stream_in)
     return res, replay
+
+
+def _hbm_probe(torch, gib=4, reps=20):
+    """Context for the roofline: what plain device operations reach on this
+    GPU.  A bf16 sum over a `gib` GiB buffer (reads only) and a copy between
+    two such buffers (reads and writes), each timed with events over `reps`
+    back-to-back launches after a warm-up; the buffers are 16x the last-level
+    cache, so every launch streams from HBM."""
+    n = gib * (1 << 30) // 2
+    x = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(x)
+    out = {}
+    for name, fn, nbytes in (("sum_read", lambda: x.sum(dtype=torch.float32), 2 * n),
+                             ("copy", lambda: y.copy_(x), 4 * n)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 1e3 / reps
+        out[name] = {"gb_per_s": round(nbytes / t / 1e9, 1), "frac_of_hbm_peak": round(nbytes / t / 1e9 / HBM_PEAK_GBPS, 4)}
+    del x, y
+    out["note"] = f"torch ops on {gib} GiB bf16 buffers, {reps} launches each; context, not a target"
+    return out
 
 
 def _cpu_sched_baseline(replay):
