@@ -5,7 +5,9 @@ sub-batches for sampled checks, and the tolerance rule.
 Tolerance (bf16 inputs, fp32 accumulation): max abs error 1e-2 and max rel
 error 5e-3.  Relative error is taken against max(|ref|, rho) with rho the
 RMS of that (row, head) reference vector, so that entries near zero do not
-divide by ~0.  The decode tests also check the fixed floor max(|ref|, 1e-3)
+divide by ~0.  The absolute bound applies to entries with |ref| < 4: from 4
+on, bf16 values are 2^-5 apart, so even the correctly rounded output can be
+1.6e-2 away, and there the relative bound (5e-3 |ref| >= 2e-2) governs.  The decode tests also check the fixed floor max(|ref|, 1e-3)
 (decode keeps P in fp32, or as bf16 high + low parts of ~16 significant bits
 on the matrix cores).  A bf16 output alone contributes up to 2^-8 = 3.9e-3
 relative error (8 significant bits, round to nearest), so that floor leaves
@@ -23,6 +25,7 @@ from paper_2504_09345_amd import workloads as W
 
 MAX_ABS = 1e-2
 MAX_REL = 5e-3
+ABS_RANGE = 4.0  # entries checked against MAX_ABS: |ref| below this
 
 
 def announce(msg: str) -> None:
@@ -101,9 +104,14 @@ def parity_stats(gpu: np.ndarray, ref: np.ndarray) -> dict:
     r = ref.astype(np.float64)
     err = np.abs(g - r)
     rho = np.sqrt((r * r).mean(axis=-1, keepdims=True))
+    # the absolute bound is checked where a bf16 output can meet it: below
+    # |ref| = 4 the bf16 grid is at most 2^-7 from any value, from 4 on its
+    # half-spacing is 2^-6 > 1e-2 and the relative bound (then >= 2e-2) governs
+    small = np.abs(r) < ABS_RANGE
     return dict(
         finite=bool(np.isfinite(g).all()),
-        max_abs=float(err.max(initial=0.0)),
+        max_abs=float(err[small].max(initial=0.0)),
+        max_abs_all=float(err.max(initial=0.0)),
         max_rel=float((err / np.maximum(np.abs(r), np.maximum(rho, 1e-30))).max(initial=0.0)),
         max_rel_floor=float((err / np.maximum(np.abs(r), 1e-3)).max(initial=0.0)),
         max_rel_global=float(err.max(initial=0.0) / max(np.abs(r).max(initial=0.0), 1e-30)),
