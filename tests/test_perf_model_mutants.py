@@ -28,6 +28,12 @@ MUTANTS = [
     ("eq12_prologue_not_halved", "(K * p - (tp + T_gpu_iter) / 2.0 * g) / tp",
      "(K * p - (tp + T_gpu_iter) * g) / tp"),
     ("eq12_one_ramp", "return 2.0 * g + (K * p", "return 1.0 * g + (K * p"),
+    ("eq6_drops_factor_two", "return 2.0 * s * I_attn * B_kv", "return s * I_attn * B_kv"),
+    ("eq6_drops_group_size", "return 2.0 * s * I_attn * B_kv", "return 2.0 * I_attn * B_kv"),
+    ("t_gpu_times_delta", "T_gpu = n_sat / dlt", "T_gpu = n_sat * dlt"),
+    ("b_kv_times_delta", 'B_kv = inp["kv_capacity_bytes"] / dlt', 'B_kv = inp["kv_capacity_bytes"] * dlt'),
+    ("delta_eff_uses_min", 'd_eff = max(dlt, inp["kv_capacity_bytes"] / inp["attn_bw"])',
+     'd_eff = min(dlt, inp["kv_capacity_bytes"] / inp["attn_bw"])'),
 ]
 
 

@@ -143,3 +143,91 @@ def test_evaluate_is_consistent():
     o2 = pm.evaluate(dict(inp, attn_bw=o["kv_bw"] / 2))
     assert o2["attn_headroom"] == pytest.approx(0.5) and o2["t_attn_bound"] == pytest.approx(o["t"] / 2)
     assert math.isfinite(o["iterations"])
+
+
+def _counted_decode_attention(n_tokens, s, D, seed=0):
+    """A small decode attention written out as the paper's CPU kernel does it
+    (Sec. 5.3: a dot product of the query with each key, then a saxpby of the
+    weighted value into the output), over bf16 K/V widened to fp32, counting
+    every floating-point multiply and add of those two operations and every
+    byte the kernel reads from the cache (the bf16 bytes) and computes on (the
+    widened fp32 bytes).  The exp of the softmax is a per-token scalar and not
+    part of the paper's intensity (dot products and saxpby only)."""
+    import random
+    rnd = random.Random(seed)
+    K = [[rnd.uniform(-1, 1) for _ in range(D)] for _ in range(n_tokens)]
+    V = [[rnd.uniform(-1, 1) for _ in range(D)] for _ in range(n_tokens)]
+    flops = 0
+    for _h in range(s):  # the s query heads of one GQA group share this KV head
+        q = [rnd.uniform(-1, 1) for _ in range(D)]
+        m, l, o = -math.inf, 0.0, [0.0] * D
+        for t in range(n_tokens):
+            x = 0.0
+            for d in range(D):  # dot product: one multiply, one add per element
+                x += q[d] * K[t][d]
+                flops += 2
+            m_new = max(m, x)
+            a, w = math.exp(m - m_new) if m > -math.inf else 0.0, math.exp(x - m_new)
+            for d in range(D):  # saxpby o = a o + w v: rescale folded into the add
+                o[d] = a * o[d] + w * V[t][d]
+                flops += 2
+            l, m = a * l + w, m_new
+    bf16_bytes = n_tokens * 2 * D * 2  # K and V, read once for the whole group
+    fp32_bytes_per_query = n_tokens * 2 * D * 4  # what one query computes on
+    return flops, bf16_bytes, fp32_bytes_per_query
+
+
+def test_eq6_equals_the_counted_flops_of_a_decode_attention():
+    """Eq. 6 (T_CPU = 2 s I B_KV) against an operation count: one query
+    attending to a KV head performs 4 D FLOPs per token (dot product and
+    saxpby) on 2 D fp32 values (8 D bytes once bf16 is up-converted), so
+    I_cpu_attn = 1/2; the s heads of a group share the KV bytes, of which the
+    cache holds 4 D bf16 bytes per token.  The FLOP rate needed to consume
+    B_KV bf16 bytes per second is then the counted FLOPs per bf16 byte times
+    B_KV, and Eq. 6 must give the same number."""
+    for n, s, D in ((5, 4, 8), (3, 6, 16), (7, 1, 4), (2, 8, 12)):
+        flops, kv_bytes, fp32_bytes = _counted_decode_attention(n, s, D)
+        I_attn = (flops / s) / fp32_bytes  # one query's FLOPs per fp32 byte
+        assert I_attn == 0.5
+        B_kv = 40e9
+        assert pm.attn_flops_required(s, I_attn, B_kv) == pytest.approx(flops / kv_bytes * B_kv, rel=1e-15)
+        # s FLOPs per cached bf16 byte
+        assert flops / kv_bytes == s
+
+
+def test_eq6_sec53_example_is_hundreds_of_gflops():
+    """Sec. 5.3: a KV cache twice the weights needs B_Mem = 3 B_IO = 60 GB/s,
+    of which B_KV = 40 GB/s streams the cache; at Mixtral's s = 4 and the
+    flash-attention intensity of 1/2 FLOP per fp32 byte, Eq. 6 asks for
+    160 GFLOP/s, 'on the order of hundreds of GFLOPs'."""
+    w, B_io = 94e9, 20e9
+    B_kv = pm.mem_bandwidth(3 * w, w, B_io) - B_io
+    assert B_kv == pytest.approx(40e9, rel=1e-12)
+    T_cpu = pm.attn_flops_required(4, 0.5, B_kv)
+    assert T_cpu == pytest.approx(160e9, rel=1e-12)
+    assert 100e9 <= T_cpu < 1000e9
+
+
+def test_evaluate_hand_worked_compositions():
+    """evaluate() composes the equations: C_GPU = 100 TFLOP/s over
+    B_IO = 25 GB/s at N_e / N_k = 4 saturates at n = 16,000 tokens (Eq. 2);
+    50 GB of weights take delta = 2 s to move, so T_GPU = n / delta =
+    8,000 tokens/s; a 100 GB cache read once per iteration is
+    B_KV = 100 GB / 2 s = 50 GB/s, and Eq. 6 at s = 4, I = 1/2 asks for
+    200 GFLOP/s; 100 GB of 128 KiB tokens are 762,939.45 tokens."""
+    inp = dict(N_e=8, N_k=2, h=4096, h_i=14336, s=4, model_bytes=50e9, kv_bytes_per_token=131072,
+               C_gpu=100e12, B_io=25e9, kv_capacity_bytes=100e9, attn_bw=0, p=100, g=32, K=10000,
+               b=16, I_attn=0.5)
+    o = pm.evaluate(inp)
+    assert o["tokens_to_saturate"] == pytest.approx(16000, rel=1e-15)
+    assert o["delta"] == pytest.approx(2.0, rel=1e-15)
+    assert o["t_gpu"] == pytest.approx(8000, rel=1e-15)
+    assert o["kv_bw"] == pytest.approx(50e9, rel=1e-15)
+    assert o["attn_flops"] == pytest.approx(200e9, rel=1e-15)
+    assert o["kv_tokens"] == pytest.approx(100e9 / 131072, rel=1e-15)
+    assert o["kv_blocks"] == math.floor(100e9 / 131072 / 16)
+    # an attention reading 25 GB/s (half of B_KV) stretches each iteration
+    # to 100 GB / 25 GB/s = 4 s, halving the token rate
+    o2 = pm.evaluate(dict(inp, attn_bw=25e9))
+    assert o2["delta_eff"] == pytest.approx(4.0, rel=1e-15)
+    assert o2["attn_headroom"] == pytest.approx(0.5, rel=1e-15)
