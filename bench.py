@@ -224,7 +224,9 @@ def main():
     ap.add_argument("--cpu-baseline-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hbm-probe", action="store_true",
-                    help="also time plain device reads and copies of multi-GB buffers (context only)")
+                    help="also time the library's read-stream probe (pa_read_probe: the decode "
+                         "kernels' load pattern, sequential and random pages) over a 4 GiB buffer: "
+                         "the access pattern's ceiling, context for the roofline")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB before timing "
                          "(a known-size kernel for scaling profiler byte counters)")
@@ -495,31 +497,53 @@ def _sched_bench(torch, batch, steps, seed):
     return res, replay
 
 
-def _hbm_probe(torch, gib=4, reps=20):
-    """Context for the roofline: what plain device operations reach on this
-    GPU.  A bf16 sum over a `gib` GiB buffer (reads only) and a copy between
-    two such buffers (reads and writes), each timed with events over `reps`
-    back-to-back launches after a warm-up; the buffers are 16x the last-level
-    cache, so every launch streams from HBM."""
-    n = gib * (1 << 30) // 2
-    x = torch.ones(n, dtype=torch.bfloat16, device="cuda")
-    y = torch.empty_like(x)
+def _hbm_probe(torch, gib=4, reps=10):
+    """The read-stream ceiling of the attention kernels' access pattern on this
+    GPU: the library's probe kernel (pa_read_probe) reads a `gib` GiB buffer
+    (16x the last-level cache, so every launch streams from HBM) in 4 KiB
+    slices with the decode kernels' loads, on the decode kernel's grid (13/16
+    of the CUs) and on all CUs: sequentially; as randomly placed 32 KiB
+    chunks (one page of 8 KV heads, as the stream-K kernel reads them) with
+    the non-temporal policy the kernels use and with the default policy; and
+    as randomly placed 4 KiB tiles.  Events over `reps` back-to-back launches
+    after a warm-up."""
+    n = gib * (1 << 30)
+    buf = torch.empty(n, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    grids = {"decode_grid": cus * 13 // 16, "all_cus": cus}
+    sink = torch.empty(max(grids.values()) * 512, dtype=torch.int32, device="cuda")
+    rng = np.random.default_rng(0)
     out = {}
-    for name, fn, nbytes in (("sum_read", lambda: x.sum(dtype=torch.float32), 2 * n),
-                             ("copy", lambda: y.copy_(x), 4 * n)):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        t = e0.elapsed_time(e1) / 1e3 / reps
-        out[name] = {"gb_per_s": round(nbytes / t / 1e9, 1), "frac_of_hbm_peak": round(nbytes / t / 1e9 / HBM_PEAK_GBPS, 4)}
-    del x, y
-    out["note"] = f"torch ops on {gib} GiB bf16 buffers, {reps} launches each; context, not a target"
+    for name, chunk, order, nt in (("sequential_nt", 32768, None, 1),
+                                   ("random_32k_nt", 32768, "perm", 1),
+                                   ("random_32k_default", 32768, "perm", 0),
+                                   ("random_4k_nt", 4096, "perm", 1)):
+        n_chunks = n // chunk
+        offs = None
+        if order == "perm":
+            o = rng.permutation(n_chunks).astype(np.int64) * chunk
+            assert o.max() + chunk <= n  # every chunk inside the buffer
+            offs = torch.from_numpy(o).cuda()
+        row = {}
+        for gname, grid in grids.items():
+            for _ in range(2):
+                pb.pa_read_probe(buf, chunk, offs, n_chunks, grid, nt, sink)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                pb.pa_read_probe(buf, chunk, offs, n_chunks, grid, nt, sink)
+            e1.record()
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / 1e3 / reps
+            row[gname] = {"grid": grid, "gb_per_s": round(n / t / 1e9, 1),
+                          "frac_of_hbm_peak": round(n / t / 1e9 / HBM_PEAK_GBPS, 4)}
+        out[name] = row
+        del offs
+    del buf, sink
+    out["note"] = (f"pa_read_probe over a {gib} GiB buffer, 4 KiB slices, 8 waves per workgroup, "
+                   f"{reps} launches each: the access pattern's ceiling, context for the roofline")
     return out
 
 
@@ -543,7 +567,7 @@ MI355X_BF16_FLOPS = 2.5e15  # dense bf16 matrix peak
 MI355X_HBM_BYTES = 288e9
 
 
-def _perf_model_leg(torch, attn_bw):
+def _perf_model_leg(torch, attn_bw, keep_raw=False):
     """The paper's Sec. 5 model (Eqs. 1-14) with the KV cache and its attention
     on one MI355X: Mixtral-8x7B (94 GB of bf16 weights, Sec. 7) streamed from
     host memory once per iteration at the measured pinned host-to-device rate
@@ -569,13 +593,16 @@ def _perf_model_leg(torch, attn_bw):
     base = dict(num_experts=8, top_k=2, model_dim=4096, expert_dim=14336, gqa_group=4,
                 model_bytes=94e9, kv_bytes_per_token=131072, gemm_flops=MI355X_BF16_FLOPS,
                 io_bw=b_io, kv_capacity_bytes=MI355X_HBM_BYTES - 32e9, attn_bw=attn_bw,
-                attn_intensity=1.0, batch=1.0, prompt=98, block=16)
+                attn_intensity=0.5, batch=1.0, prompt=98, block=16)
     out = {"model": "mixtral-8x7b", "io_bw_measured_gb_s": round(b_io / 1e9, 2),
            "attn_bw_measured_gb_s": round(attn_bw / 1e9, 1), "kv_capacity_gb": 256.0,
            "gemm_tflops": MI355X_BF16_FLOPS / 1e12, "cases": []}
+    raw = []
     for g in (32, 128):
         q = pb.pa_perf_model(**dict(base, gen=g))["q"]
-        r = pb.pa_perf_model(**dict(base, gen=g, batch=5 * g * q))
+        inp = dict(base, gen=g, batch=5 * g * q)
+        r = pb.pa_perf_model(**inp)
+        raw.append((inp, r))
         out["cases"].append({
             "prompt": 98, "gen": g, "batch_K": round(5 * g * q),
             "tokens_to_saturate": round(r["tokens_to_saturate"]), "delta_s": round(r["delta"], 3),
@@ -587,6 +614,8 @@ def _perf_model_leg(torch, attn_bw):
             "kv_bw_needed_gb_s": round(r["kv_bw"] / 1e9, 2),
             "attn_headroom": round(r["attn_headroom"], 1),
             "t_with_measured_attention_tok_s": round(r["t_attn_bound"], 1)})
+    if keep_raw:
+        out["raw"] = raw
     return out
 
 
@@ -601,7 +630,7 @@ MODEL_GEMMS = {
 }
 
 
-def _overlap_gemm(torch, batch, dev_q, k, v, bt, cl, scale, reps, workload):
+def _overlap_gemm(torch, batch, dev_q, k, v, bt, cl, scale, reps, workload, keep_output=False):
     """Two partitions of the decode batch, as in the paper's pipelined engine
     (Sec. 6.4): attention of partition alpha (first half of the sequences) runs
     on one stream while the layer GEMMs of partition beta (QKV and output
@@ -687,6 +716,8 @@ def _overlap_gemm(torch, batch, dev_q, k, v, bt, cl, scale, reps, workload):
         "attn_slowdown_in_overlap": round(med(ca) / med(ga), 3),
         "attn_bit_identical_under_overlap": same,
     })
+    if keep_output:
+        res["out_alpha"] = out_a.float().cpu().numpy()
     return res
 
 

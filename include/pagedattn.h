@@ -115,8 +115,8 @@ typedef struct pa_timing {
 
 /* Bytes of device workspace a paged_attn / paged_attn_varlen call with these
  * dims needs: partial outputs and softmax statistics of items split across
- * workgroups, and per-workgroup flags that publish them.  Writes 0 when no workspace
- * is needed.  A call whose dims carry chunked rows (max_q_len > 1 or
+ * workgroups, and the arrival counters of those items.  Writes 0 when no
+ * workspace is needed.  A call whose dims carry chunked rows (max_q_len > 1 or
  * num_q_rows != num_seqs) is sized as varlen.  Host only; no HIP call.
  * Errors: PA_EINVAL / PA_ENOTSUP as for paged_attn. */
 int pa_workspace_size(const pa_dims_t *dims, size_t *bytes);
@@ -124,9 +124,11 @@ int pa_workspace_size(const pa_dims_t *dims, size_t *bytes);
 /* Decode attention: one query row per sequence (Sec. 6.6 computes exactly
  * this on the CPU).  Here: a persistent stream-K kernel over equal ranges of
  * (sequence, KV-head block, page) units whose workgroups also merge the
- * items cut by range boundaries (one launch); with pages_per_split > 0, or
- * more than 8192 sequences, a per-row split-K kernel plus a reduction kernel.
- * Both are deterministic (no float atomics; merges run in a fixed order).
+ * items cut by range boundaries (one launch: the last part of a cut item to
+ * finish merges it, so no workgroup ever waits for another); with
+ * pages_per_split > 0, or more than 8192 sequences, a per-row split-K kernel
+ * plus a reduction kernel.  Both are deterministic (no float atomics; merges
+ * run in a fixed order).
  *   q            [num_seqs][H_q][D]        device, read
  *   k_pages,
  *   v_pages      pool, see layouts above   device, read
@@ -162,18 +164,31 @@ int paged_attn_varlen(const void *q, const void *k_pages, const void *v_pages,
                       const pa_dims_t *dims, void *workspace, size_t workspace_bytes,
                       hipStream_t stream, const pa_timing_t *timing);
 
-/* Block-table gather trace: for every cached token, sequence-major, the flat
- * pool row page * page_size + slot that the attention kernels read for it
- * (computed by the same device address function the kernels use).
- *   rows_out  int64 device array of sum_b context_lens[b] entries; sequence b
- *             starts at sum_{b' < b} context_lens[b'].
- *   row_start int64 device array of num_seqs entries holding those starts
- *             (the caller computes them; the library does not scan).
- * Uses num_seqs, page_size, max_pages_per_seq, max_context_len of dims.
- * Errors: PA_EINVAL, PA_ENOTSUP, PA_EHIP. */
-int pa_gather_trace(const int32_t *block_table, const int32_t *context_lens,
-                    const int64_t *row_start, const pa_dims_t *dims, int64_t *rows_out,
-                    hipStream_t stream);
+/* Block-table gather trace (Sec. 5.5 paging; Sec. 2 GQA): the same call as
+ * paged_attn (query_start_loc == NULL) or paged_attn_varlen (otherwise), run
+ * through instantiations of the very same kernels that also record, for every
+ * token they load, the pool row its K and V came from.  `out` is written
+ * exactly as the attention call writes it.  The record is taken from the
+ * element offset each kernel hands to its tile loads, so it checks the
+ * kernels' own block-table gather (the stream-K unit table, the prefill
+ * kernel's block-table window, the split-K kernel's per-lane entries), not a
+ * separate address function.
+ *   rows_out  int64 device array [num_kv_heads][num_seqs][max_pages_per_seq * 16],
+ *             filled by the call: entry (g, b, t) is the row
+ *             (page * num_kv_heads + g) * 16 + t % 16 of the
+ *             [num_pages][num_kv_heads][16] pool, page = block_table[b][t / 16],
+ *             from which some kernel loaded token t of sequence b for KV head
+ *             g; -1 where no kernel loaded the token (t >= context_lens[b]),
+ *             -2 where two loads of the token came from different rows.
+ * Other arguments, layouts, workspace and errors as for paged_attn /
+ * paged_attn_varlen (rows_out == NULL with query rows: PA_EINVAL).  Meant
+ * for tests: the trace instantiations run somewhat slower than the
+ * attention kernels. */
+int pa_gather_trace(const void *q, const void *k_pages, const void *v_pages,
+                    const int32_t *block_table, const int32_t *context_lens,
+                    const int32_t *query_start_loc, float scale, void *out,
+                    const pa_dims_t *dims, void *workspace, size_t workspace_bytes,
+                    int64_t *rows_out, hipStream_t stream);
 
 /* KV append: store the new tokens' keys and values into the paged cache, the
  * step right before attention (Sec. 6.4: the task that receives a decode

@@ -21,7 +21,7 @@ PA_BF16, PA_FP32 = 0, 1
 PAGE_SIZE = 16
 
 EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "pa_gather_trace",
-            "pa_kv_append", "pa_schedule_step", "pa_perf_model", "pa_strerror")
+            "pa_kv_append", "pa_schedule_step", "pa_perf_model", "pa_read_probe", "pa_strerror")
 
 
 class PaDims(ctypes.Structure):
@@ -104,7 +104,7 @@ def load():
     lib.paged_attn.restype = ctypes.c_int
     lib.paged_attn_varlen.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, DP, P, SZ, P, TP]
     lib.paged_attn_varlen.restype = ctypes.c_int
-    lib.pa_gather_trace.argtypes = [P, P, P, DP, P, P]
+    lib.pa_gather_trace.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, DP, P, SZ, P, P]
     lib.pa_gather_trace.restype = ctypes.c_int
     lib.pa_kv_append.argtypes = [P, P, P, P, P, P, P, DP, P]
     lib.pa_kv_append.restype = ctypes.c_int
@@ -113,6 +113,8 @@ def load():
     lib.pa_schedule_step.restype = ctypes.c_int
     lib.pa_perf_model.argtypes = [ctypes.POINTER(PaPmInput), ctypes.POINTER(PaPmOutput)]
     lib.pa_perf_model.restype = ctypes.c_int
+    lib.pa_read_probe.argtypes = [P, ctypes.c_int64, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P]
+    lib.pa_read_probe.restype = ctypes.c_int
     lib.pa_strerror.argtypes = [ctypes.c_int]
     lib.pa_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -171,11 +173,21 @@ def pa_strerror(code: int) -> str:
     return load().pa_strerror(int(code)).decode()
 
 
-def _workspace(dims, workspace, device):
+def _workspace(dims, workspace, device, stream=None):
+    """The caller's workspace, or a temporary one of pa_workspace_size()
+    bytes.  A temporary is allocated on torch's current stream; when the call
+    runs on another stream, the allocation is also recorded on that stream, so
+    torch's caching allocator does not hand the memory to other work before
+    the call's kernels have finished with it."""
     need = pa_workspace_size(dims)
     if workspace is None and need > 0:
         import torch
+        if isinstance(stream, int) and stream:
+            # torch cannot track work on a raw stream handle
+            raise ValueError("pass a workspace (or a torch stream) when calling on a raw stream handle")
         workspace = torch.empty(need, dtype=torch.uint8, device=device)
+        if stream is not None and stream != torch.cuda.current_stream(workspace.device):
+            workspace.record_stream(stream)
     size = 0 if workspace is None else (workspace.numel() * workspace.element_size()
                                         if hasattr(workspace, "numel") else need)
     return workspace, size
@@ -184,7 +196,7 @@ def _workspace(dims, workspace, device):
 def paged_attn(q, k_pages, v_pages, block_table, context_lens, scale, out, dims: PaDims,
                workspace=None, stream=None, timing: PaTiming | None = None, check=True) -> int:
     """int paged_attn(...): decode attention; out is written in place."""
-    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None))
+    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None), stream)
     rc = load().paged_attn(_addr(q), _addr(k_pages), _addr(v_pages), _addr(block_table),
                            _addr(context_lens), float(scale), _addr(out), ctypes.byref(dims),
                            _addr(ws), ws_bytes, _stream(stream),
@@ -198,7 +210,7 @@ def paged_attn_varlen(q, k_pages, v_pages, block_table, context_lens, query_star
                       dims: PaDims, workspace=None, stream=None, timing: PaTiming | None = None,
                       check=True) -> int:
     """int paged_attn_varlen(...): causal prefill chunks plus decode rows."""
-    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None))
+    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None), stream)
     rc = load().paged_attn_varlen(_addr(q), _addr(k_pages), _addr(v_pages), _addr(block_table),
                                   _addr(context_lens), _addr(query_start_loc), float(scale),
                                   _addr(out), ctypes.byref(dims), _addr(ws), ws_bytes,
@@ -209,11 +221,17 @@ def paged_attn_varlen(q, k_pages, v_pages, block_table, context_lens, query_star
     return rc
 
 
-def pa_gather_trace(block_table, context_lens, row_start, dims: PaDims, rows_out, stream=None,
-                    check=True) -> int:
-    """int pa_gather_trace(...): pool row of every cached token."""
-    rc = load().pa_gather_trace(_addr(block_table), _addr(context_lens), _addr(row_start),
-                                ctypes.byref(dims), _addr(rows_out), _stream(stream))
+def pa_gather_trace(q, k_pages, v_pages, block_table, context_lens, scale, out, dims: PaDims,
+                    rows_out, query_start_loc=None, workspace=None, stream=None, check=True) -> int:
+    """int pa_gather_trace(...): the attention call (decode, or varlen when
+    query_start_loc is given) through the kernels' trace instantiations;
+    rows_out [H_kv][B][max_pages_per_seq * 16] int64 receives the pool row of
+    every loaded token."""
+    ws, ws_bytes = _workspace(dims, workspace, getattr(q, "device", None), stream)
+    rc = load().pa_gather_trace(_addr(q), _addr(k_pages), _addr(v_pages), _addr(block_table),
+                                _addr(context_lens), _addr(query_start_loc), float(scale),
+                                _addr(out), ctypes.byref(dims), _addr(ws), ws_bytes,
+                                _addr(rows_out), _stream(stream))
     if check and rc != PA_OK:
         raise PagedAttnError("pa_gather_trace", rc)
     return rc
@@ -239,6 +257,17 @@ def pa_schedule_step(state: PaSchedState, n_real, new_seq, new_prompt, new_fin, 
                                  _stream(stream))
     if check and rc != PA_OK:
         raise PagedAttnError("pa_schedule_step", rc)
+    return rc
+
+
+def pa_read_probe(buf, chunk_bytes, chunk_offsets, n_chunks, grid, non_temporal, sink, stream=None,
+                  check=True) -> int:
+    """int pa_read_probe(...): read n_chunks chunks of buf with the decode
+    kernels' load pattern (include/pa_probe.h)."""
+    rc = load().pa_read_probe(_addr(buf), int(chunk_bytes), _addr(chunk_offsets), int(n_chunks), int(grid),
+                              int(non_temporal), _addr(sink), _stream(stream))
+    if check and rc != PA_OK:
+        raise PagedAttnError("pa_read_probe", rc)
     return rc
 
 

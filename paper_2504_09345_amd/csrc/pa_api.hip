@@ -101,12 +101,16 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
     const size_t recs = (size_t)pa::kStreamMaxGrid * 2 * p->W * s;  // (workgroup, slot, wave, head)
     p->st_o = align256(recs * (size_t)d->head_dim * sizeof(float));
     p->st_ml = align256(recs * 2 * sizeof(float));
-    p->st_cum = align256((size_t)pa::kStreamMaxGrid * sizeof(unsigned long long));  // range flags
+    // arrival counters of cut items: one per (first range, wave)
+    p->st_cum = align256((size_t)pa::kStreamMaxGrid * p->W * sizeof(unsigned long long));
   }
   // chunked-prefill rows of a varlen call: MFMA kernel (bf16, head_dim 128)
   p->prefill = varlen && p->stream && pa::prefill_supported(d->dtype, d->head_dim, s);
-  // split-K for whatever the stream and prefill paths do not take
-  p->split = varlen ? (rows > 0 && !p->prefill) : !p->stream;
+  // split-K for whatever the stream and prefill paths do not take: in a
+  // varlen call, chunk rows the MFMA kernel cannot take (there are none when
+  // max_q_len <= 1: every row is then a decode row, which the stream kernel
+  // takes)
+  p->split = varlen ? (rows > 0 && !p->prefill && (d->max_q_len > 1 || !p->stream)) : !p->stream;
   p->pps = d->pages_per_split > 0 ? d->pages_per_split : kDefaultPagesPerSplit;
   p->n_split_slots = (int)((max_pages + p->pps - 1) / p->pps);
   if (p->n_split_slots < 1) p->n_split_slots = 1;
@@ -142,10 +146,12 @@ void record(hipEvent_t ev, hipStream_t st) {
   if (ev != nullptr) (void)hipEventRecord(ev, st);
 }
 
+// One attention call.  trace: nullptr, or the gather trace's array (the
+// kernels' trace instantiations then also record every loaded token's row).
 int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
         const int32_t* context_lens, const int32_t* query_start_loc, float scale, void* out,
         const pa_dims_t* dims, void* workspace, size_t workspace_bytes, hipStream_t stream,
-        const pa_timing_t* timing, bool varlen) {
+        const pa_timing_t* timing, bool varlen, int64_t* trace = nullptr) {
   Plan p;
   int rc = plan(dims, varlen, &p);
   if (rc != PA_OK) return rc;
@@ -184,6 +190,9 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     // batch 256 213-214 us per launch at 208 workgroups, 214-217 at 192, 218
     // at 256, 231 at 160; DBRX and 32k contexts within 0.5 % from 192 to 208,
     // 1-2 % slower at 256.
+    // A batch whose ranges would overflow the LDS unit table takes more
+    // workgroups (up to kStreamMaxGrid), even beyond one wave of resident
+    // workgroups: no workgroup waits for another, so any residency works.
     int64_t g = (int64_t)per_cu * cus * kStreamCuNum / kStreamCuDen;
     if (g < 1) g = 1;
     if (g < p.g_min) g = p.g_min;
@@ -207,6 +216,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     sa.H_kv = dims->num_kv_heads;
     sa.max_context_len = dims->max_context_len;
     sa.nb = p.nb;
+    sa.trace = trace;
   }
   // Mixed batch: decode and prefill workgroups side by side in one launch,
   // unless the chunk rows outweigh the decode rows.  A decode row streams its
@@ -260,6 +270,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     pf.H_q = dims->num_q_heads;
     pf.H_kv = dims->num_kv_heads;
     pf.max_context_len = dims->max_context_len;
+    pf.trace = trace;
     if (mixed) {
       // a quarter of the CUs for the chunks, the rest (at most the decode
       // grid) for the decode rows: one grid of one workgroup per CU
@@ -296,6 +307,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     a.pages_per_split = p.pps;
     a.n_split_slots = p.n_split_slots;
     a.skip_single_rows = p.stream ? 1 : 0;
+    a.trace = trace;
     e = pa::launch_decode(dims->dtype, dims->head_dim, p.s, a, p.rows, stream, next_events());
     if (e != hipSuccess) return PA_EHIP;
   }
@@ -359,19 +371,25 @@ int paged_attn_varlen(const void* q, const void* k_pages, const void* v_pages,
              workspace, workspace_bytes, stream, timing, true);
 }
 
-int pa_gather_trace(const int32_t* block_table, const int32_t* context_lens,
-                    const int64_t* row_start, const pa_dims_t* dims, int64_t* rows_out,
+int pa_gather_trace(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+                    const int32_t* context_lens, const int32_t* query_start_loc, float scale, void* out,
+                    const pa_dims_t* dims, void* workspace, size_t workspace_bytes, int64_t* rows_out,
                     hipStream_t stream) {
-  if (dims == nullptr) return PA_EINVAL;
-  if (dims->num_seqs < 0 || dims->max_context_len < 0 || dims->max_pages_per_seq < 0)
-    return PA_EINVAL;
-  if (dims->page_size != 16) return PA_ENOTSUP;
-  if ((dims->max_context_len + 15) / 16 > dims->max_pages_per_seq) return PA_EINVAL;
-  if (dims->num_seqs == 0 || dims->max_context_len == 0) return PA_OK;
-  if (!block_table || !context_lens || !row_start || !rows_out) return PA_EINVAL;
-  hipError_t e = pa::launch_gather_trace(block_table, dims->max_pages_per_seq, context_lens, row_start,
-                                         dims->num_seqs, dims->max_context_len, rows_out, stream);
-  return e == hipSuccess ? PA_OK : PA_EHIP;
+  const bool varlen = query_start_loc != nullptr;
+  Plan p;
+  int rc = plan(dims, varlen, &p);
+  if (rc != PA_OK) return rc;
+  if (p.rows == 0) return run(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out, dims,
+                              workspace, workspace_bytes, stream, nullptr, varlen);
+  if (rows_out == nullptr) return PA_EINVAL;
+  const int64_t n = (int64_t)dims->num_kv_heads * dims->num_seqs * dims->max_pages_per_seq * 16;
+  // the attention call's own validation runs before anything is enqueued
+  if (!isfinite(scale) || !(scale > 0.0f)) return PA_EINVAL;
+  if (!q || !k_pages || !v_pages || !block_table || !context_lens || !out) return PA_EINVAL;
+  if (p.ws_bytes > 0 && (workspace == nullptr || workspace_bytes < p.ws_bytes)) return PA_ENOSPC;
+  if (pa::launch_fill_i64(rows_out, n, -1, stream) != hipSuccess) return PA_EHIP;
+  return run(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out, dims, workspace,
+             workspace_bytes, stream, nullptr, varlen, rows_out);
 }
 
 int pa_kv_append(const void* k_new, const void* v_new, const int32_t* block_table,

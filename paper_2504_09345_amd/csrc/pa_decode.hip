@@ -31,7 +31,9 @@
 
 namespace pa {
 
-template <typename T, int D, int S, int WAVES, int NBUF>
+// TR: gather-trace instantiation (records every loaded token's pool row in
+// a.trace besides computing the attention).
+template <typename T, int D, int S, int WAVES, int NBUF, bool TR>
 __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeArgs a) {
   using Sh = DecodeShape<T, D, S>;
   constexpr int NT = 64 * WAVES;
@@ -102,6 +104,10 @@ __global__ __launch_bounds__(64 * WAVES) void decode_kernel(DecodeArgs a) {
       const int32_t page = __builtin_amdgcn_readlane(bt_lane, kk);
       off = tile_offset(page, g, a.H_kv, D);
       valid = min(kPage, ctx - p * kPage);
+      if constexpr (TR) {
+        if (lane < valid)
+          trace_put(a.trace, ((int64_t)g * a.B + b) * (a.bt_stride * kPage) + p * kPage + lane, off / D + lane);
+      }
     }
     issue_tile<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), tile_rsrc<T, D>(vp + off, valid), lane_off, kr, vr);
   };
@@ -201,38 +207,30 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
   for (int e = 0; e < E; ++e) store_out<T>(out + lane * E + e, acc[e] / L);
 }
 
-// Gather trace: rows_out[row_start[b] + t] = pool row of token t of sequence b,
-// through the same BlockTable / pool_row functions the attention kernels use.
-__global__ __launch_bounds__(256) void gather_trace_kernel(BlockTable bt, const int32_t* context_lens,
-                                                           const int64_t* row_start, int64_t* rows_out) {
-  const int b = blockIdx.y;
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  const int ctx = context_lens[b];
-  if (t >= ctx) return;
-  // a context longer than the block-table row is a contract violation: -1
-  rows_out[row_start[b] + t] = t / kPage < bt.stride ? pool_row(bt.page(b, t / kPage), t) : -1;
-}
-
 // ---- launchers -----------------------------------------------------------
 
-template <typename T, int D>
-static const void* decode_fn(int s) {
+template <typename T, int D, bool TR>
+static const void* decode_pick(int s) {
   switch (s) {
-    case 1: return reinterpret_cast<const void*>(&decode_kernel<T, D, 1, kDecodeWaves, kDecodeRing>);
-    case 2: return reinterpret_cast<const void*>(&decode_kernel<T, D, 2, kDecodeWaves, kDecodeRing>);
-    case 4: return reinterpret_cast<const void*>(&decode_kernel<T, D, 4, kDecodeWaves, kDecodeRing>);
-    case 6: return reinterpret_cast<const void*>(&decode_kernel<T, D, 6, kDecodeWaves, kDecodeRing>);
-    case 8: return reinterpret_cast<const void*>(&decode_kernel<T, D, 8, kDecodeWaves, kDecodeRing>);
+    case 1: return reinterpret_cast<const void*>(&decode_kernel<T, D, 1, kDecodeWaves, kDecodeRing, TR>);
+    case 2: return reinterpret_cast<const void*>(&decode_kernel<T, D, 2, kDecodeWaves, kDecodeRing, TR>);
+    case 4: return reinterpret_cast<const void*>(&decode_kernel<T, D, 4, kDecodeWaves, kDecodeRing, TR>);
+    case 6: return reinterpret_cast<const void*>(&decode_kernel<T, D, 6, kDecodeWaves, kDecodeRing, TR>);
+    case 8: return reinterpret_cast<const void*>(&decode_kernel<T, D, 8, kDecodeWaves, kDecodeRing, TR>);
   }
   return nullptr;
 }
 
+template <typename T, int D>
+static const void* decode_fn(int s, bool trace) { return trace ? decode_pick<T, D, true>(s) : decode_pick<T, D, false>(s); }
+
 hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st, KernelEvents ev) {
   const void* fn = nullptr;
-  if (dtype == 0 && D == 128) fn = decode_fn<uint16_t, 128>(s);
-  else if (dtype == 0 && D == 64) fn = decode_fn<uint16_t, 64>(s);
-  else if (dtype == 1 && D == 128) fn = decode_fn<float, 128>(s);
-  else if (dtype == 1 && D == 64) fn = decode_fn<float, 64>(s);
+  const bool tr = a.trace != nullptr;
+  if (dtype == 0 && D == 128) fn = decode_fn<uint16_t, 128>(s, tr);
+  else if (dtype == 0 && D == 64) fn = decode_fn<uint16_t, 64>(s, tr);
+  else if (dtype == 1 && D == 128) fn = decode_fn<float, 128>(s, tr);
+  else if (dtype == 1 && D == 64) fn = decode_fn<float, 64>(s, tr);
   if (fn == nullptr) return hipErrorInvalidValue;
   const int64_t n = (int64_t)rows * a.H_kv * a.n_split_slots;
   if (n == 0) return hipSuccess;
@@ -252,16 +250,6 @@ hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st) 
   else if (dtype == 1 && D == 128) reduce_kernel<float, 128><<<grid, block, 0, st>>>(a);
   else if (dtype == 1 && D == 64) reduce_kernel<float, 64><<<grid, block, 0, st>>>(a);
   else return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
-hipError_t launch_gather_trace(const int32_t* block_table, int64_t bt_stride,
-                               const int32_t* context_lens, const int64_t* row_start, int B,
-                               int max_context_len, int64_t* rows_out, hipStream_t st) {
-  if (B == 0 || max_context_len == 0) return hipSuccess;
-  const dim3 grid((max_context_len + 255) / 256, B), block(256);
-  gather_trace_kernel<<<grid, block, 0, st>>>(BlockTable{block_table, bt_stride}, context_lens,
-                                              row_start, rows_out);
   return hipGetLastError();
 }
 

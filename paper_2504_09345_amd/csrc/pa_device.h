@@ -187,18 +187,27 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp) {
   }
 }
 
+// Gather trace (instantiations with a trace array only): record the pool row
+// that a kernel loaded for token t of sequence b under KV head g at
+// trace[(g * B + b) * stride_tokens + t].  Entries start at -1; a second load
+// of the same token with a different row marks the entry -2.
+__device__ __forceinline__ void trace_put(int64_t* trace, int64_t idx, int64_t row) {
+  unsigned long long* p = reinterpret_cast<unsigned long long*>(trace + idx);
+  const unsigned long long old = atomicCAS(p, ~0ull, (unsigned long long)row);
+  if (old != ~0ull && old != (unsigned long long)row) atomicExch(p, (unsigned long long)-2ll);
+}
+
 // Block-table address function.  Token t of sequence b sits in slot t % 16 of
 // page block_table[b][t / 16]; the pool row of that token is page * 16 + slot
 // and, for KV head g of a [page][H_kv][16][D] pool, its first element is
-// ((page * H_kv + g) * 16 + slot) * D.  Every kernel (and the gather trace)
-// goes through these two functions.
+// ((page * H_kv + g) * 16 + slot) * D.  Every attention kernel goes through
+// BlockTable::page and tile_offset (or, in the prefill kernel, the same
+// offset formula over its LDS window of the table).
 struct BlockTable {
   const int32_t* table;
   int64_t stride;  // max_pages_per_seq
   __device__ __forceinline__ int32_t page(int b, int p) const { return table[(int64_t)b * stride + p]; }
 };
-
-__device__ __forceinline__ int64_t pool_row(int32_t page, int t) { return (int64_t)page * kPage + (t & (kPage - 1)); }
 
 __device__ __forceinline__ int64_t tile_offset(int32_t page, int g, int H_kv, int D) {
   return ((int64_t)page * H_kv + g) * (int64_t)(kPage * D);

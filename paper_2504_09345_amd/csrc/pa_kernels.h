@@ -32,6 +32,7 @@ struct DecodeArgs {
   int pages_per_split;
   int n_split_slots;
   int skip_single_rows;      // varlen: leave one-row sequences to the stream kernel
+  int64_t* trace;            // gather-trace launches only (see StreamArgs), else nullptr
 };
 
 struct ReduceArgs {
@@ -60,12 +61,16 @@ struct StreamArgs {
   void* out;
   float* ws_o;       // [G][2][W][s][D] partial outputs (slot 0 head, 1 tail)
   float* ws_ml;      // [G][2][W][s][2]
-  unsigned long long* ws_flag;  // [G] set to `token` once a range's head record is written
+  unsigned long long* ws_flag;  // [G][W] arrival counters of cut items, keyed by the item's first range
   unsigned long long token;     // tag of this call (never 0; differs from every earlier call's)
   int64_t bt_stride;
   float scale_log2;
   int B, H_q, H_kv, max_context_len;
   int nb;            // head blocks = H_kv / W
+  // Gather trace (nullptr in attention calls): [H_kv][B][bt_stride * 16]
+  // int64, the pool row ((page * H_kv + g) * 16 + slot) each loaded token came
+  // from; launched through the trace instantiations of the kernels.
+  int64_t* trace;
 };
 
 constexpr int kStreamMaxRows = 8192;    // sequences per call on the stream path
@@ -94,6 +99,9 @@ struct KernelEvents {
 hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st,
                          KernelEvents ev = {});
 int stream_occupancy(int dtype, int D, int s, int W);  // workgroups per CU, 0 on error
+// Stream-K kernel for (element type, head dim, trace): pick by s and W (one
+// translation unit per combination, compiled in parallel).
+template <typename T, int D, bool TR> const void* stream_pick(int s, int W);
 
 // Arguments of the MFMA chunked-prefill kernel (bf16, head_dim 128): the rows
 // of every sequence with a chunk of L > 1 query rows.
@@ -108,6 +116,7 @@ struct PrefillArgs {
   int64_t bt_stride;
   float scale_log2;
   int B, H_q, H_kv, max_context_len;
+  int64_t* trace;  // gather-trace launches only (see StreamArgs), else nullptr
 };
 
 bool prefill_supported(int dtype, int D, int s);
@@ -140,9 +149,8 @@ hipError_t launch_kv_append(const AppendArgs& a, hipStream_t st);
 hipError_t launch_decode(int dtype, int D, int s, const DecodeArgs& a, int rows, hipStream_t st,
                          KernelEvents ev = {});
 hipError_t launch_reduce(int dtype, int D, const ReduceArgs& a, hipStream_t st);
-hipError_t launch_gather_trace(const int32_t* block_table, int64_t bt_stride,
-                               const int32_t* context_lens, const int64_t* row_start, int B,
-                               int max_context_len, int64_t* rows_out, hipStream_t st);
+// Fill n int64 entries with `value` (the gather trace's starting state).
+hipError_t launch_fill_i64(int64_t* p, int64_t n, int64_t value, hipStream_t st);
 
 // Maximum pages a workgroup's split may span (block-table entries are held one
 // per lane of each wave).

@@ -8,10 +8,10 @@
 // one after the other.  Workgroups [0, G_dec) run the stream-K body over the
 // decode units exactly as the stream kernel would with a grid of G_dec
 // (including the merge of cut items); workgroups [G_dec, grid) run the
-// prefill body with a grid of grid - G_dec.  No prefill workgroup waits on
-// another, and decode workgroups only wait on higher decode ranges, so the
-// split is correct whatever the residency.  The two bodies' LDS
-// layouts share one union.
+// prefill body with a grid of grid - G_dec.  No workgroup waits on another
+// (a cut decode item is merged by whichever of its parts finishes last), so
+// the split is correct whatever the residency and dispatch order.  The two
+// bodies' LDS layouts share one union.
 #include "pa_prefill_body.h"
 #include "pa_stream_body.h"
 
@@ -30,25 +30,29 @@ union MixedSmem {
   } pf;
 };
 
-template <int S>
+template <int S, bool TR>
 __global__ __launch_bounds__(64 * kMixedW) void mixed_kernel(StreamArgs sa, PrefillArgs pa_, int G_dec) {
   __shared__ MixedSmem sm;
   if ((int)blockIdx.x < G_dec)
-    stream_body<uint16_t, mfma::kD, S, kMixedW, kStreamRing, true>(sa, sm.dec, blockIdx.x, G_dec);
+    stream_body<uint16_t, mfma::kD, S, kMixedW, kStreamRing, true, TR>(sa, sm.dec, blockIdx.x, G_dec);
   else
-    prefill_body<mfma::kD, S>(pa_, sm.pf.smem, sm.pf.cum, blockIdx.x - G_dec, gridDim.x - G_dec);
+    prefill_body<mfma::kD, S, TR>(pa_, sm.pf.smem, sm.pf.cum, blockIdx.x - G_dec, gridDim.x - G_dec);
 }
 
-const void* mixed_fn(int s) {
+template <bool TR>
+const void* mixed_pick(int s) {
   switch (s) {
-    case 1: return reinterpret_cast<const void*>(&mixed_kernel<1>);
-    case 2: return reinterpret_cast<const void*>(&mixed_kernel<2>);
-    case 4: return reinterpret_cast<const void*>(&mixed_kernel<4>);
-    case 6: return reinterpret_cast<const void*>(&mixed_kernel<6>);
-    case 8: return reinterpret_cast<const void*>(&mixed_kernel<8>);
+    case 1: return reinterpret_cast<const void*>(&mixed_kernel<1, TR>);
+    case 2: return reinterpret_cast<const void*>(&mixed_kernel<2, TR>);
+    case 4: return reinterpret_cast<const void*>(&mixed_kernel<4, TR>);
+    case 6: return reinterpret_cast<const void*>(&mixed_kernel<6, TR>);
+    case 8: return reinterpret_cast<const void*>(&mixed_kernel<8, TR>);
   }
   return nullptr;
 }
+
+// trace: the gather-trace instantiation (also records the rows it loads)
+const void* mixed_fn(int s, bool trace = false) { return trace ? mixed_pick<true>(s) : mixed_pick<false>(s); }
 
 }  // namespace
 
@@ -58,7 +62,7 @@ bool mixed_supported(int dtype, int D, int s, int W) {
 
 hipError_t launch_mixed(int s, const StreamArgs& sa, const PrefillArgs& pa_, int G_dec, int G, hipStream_t st,
                         KernelEvents ev) {
-  const void* fn = mixed_fn(s);
+  const void* fn = mixed_fn(s, sa.trace != nullptr);
   if (fn == nullptr || G_dec <= 0 || G <= G_dec) return hipErrorInvalidValue;
   StreamArgs a0 = sa;
   PrefillArgs a1 = pa_;

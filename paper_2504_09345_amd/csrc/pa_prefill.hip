@@ -43,23 +43,27 @@
 
 namespace pa {
 
-template <int D, int S>
+template <int D, int S, bool TR>
 __global__ __launch_bounds__(kPfThreads) void prefill_kernel(PrefillArgs a) {
   __shared__ PrefillSmem sm;
   extern __shared__ int32_t s_cum[];  // [B + 1] prefix of items per sequence
-  prefill_body<D, S>(a, sm, s_cum, blockIdx.x, gridDim.x);
+  prefill_body<D, S, TR>(a, sm, s_cum, blockIdx.x, gridDim.x);
 }
 
-static const void* prefill_fn(int s) {
+template <bool TR>
+static const void* prefill_pick(int s) {
   switch (s) {
-    case 1: return reinterpret_cast<const void*>(&prefill_kernel<128, 1>);
-    case 2: return reinterpret_cast<const void*>(&prefill_kernel<128, 2>);
-    case 4: return reinterpret_cast<const void*>(&prefill_kernel<128, 4>);
-    case 6: return reinterpret_cast<const void*>(&prefill_kernel<128, 6>);
-    case 8: return reinterpret_cast<const void*>(&prefill_kernel<128, 8>);
+    case 1: return reinterpret_cast<const void*>(&prefill_kernel<128, 1, TR>);
+    case 2: return reinterpret_cast<const void*>(&prefill_kernel<128, 2, TR>);
+    case 4: return reinterpret_cast<const void*>(&prefill_kernel<128, 4, TR>);
+    case 6: return reinterpret_cast<const void*>(&prefill_kernel<128, 6, TR>);
+    case 8: return reinterpret_cast<const void*>(&prefill_kernel<128, 8, TR>);
   }
   return nullptr;
 }
+
+// trace: the gather-trace instantiation (also records the rows it loads)
+static const void* prefill_fn(int s, bool trace = false) { return trace ? prefill_pick<true>(s) : prefill_pick<false>(s); }
 
 bool prefill_supported(int dtype, int D, int s) { return dtype == 0 && D == 128 && prefill_fn(s) != nullptr; }
 
@@ -73,7 +77,7 @@ int prefill_occupancy(int s, int B) {
 }
 
 hipError_t launch_prefill(int s, const PrefillArgs& a, int G, hipStream_t st, KernelEvents ev) {
-  const void* fn = prefill_fn(s);
+  const void* fn = prefill_fn(s, a.trace != nullptr);
   if (fn == nullptr || G <= 0) return hipErrorInvalidValue;
   void* args[] = {const_cast<PrefillArgs*>(&a)};
   hipError_t e = hipExtLaunchKernel(fn, dim3(G), dim3(kPfThreads), args, (size_t)(a.B + 1) * sizeof(int32_t), st,

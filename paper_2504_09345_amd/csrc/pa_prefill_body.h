@@ -42,7 +42,9 @@ struct PrefillSmem {
 };
 
 // Prefill workgroup `bid` of a grid of G; s_cum holds B + 1 ints of LDS.
-template <int D, int S>
+// TR: gather-trace instantiation (records every loaded token's pool row in
+// a.trace besides computing the attention).
+template <int D, int S, bool TR = false>
 __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& sm, int32_t* s_cum, int bid,
                                              int G) {
   static_assert(D == mfma::kD, "prefill MFMA path is built for head_dim 128");
@@ -162,6 +164,10 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
       const int32_t entry = __builtin_amdgcn_readfirstlane(s_bt[pg & (kPfMaxPages - 1)]);
       const int32_t page = pg < npg ? entry : 0;
       const int64_t tile = ((int64_t)page * a.H_kv + g) * (int64_t)(kPage * D);
+      if constexpr (TR) {
+        if (st_c == 0 && st_key < valid)
+          trace_put(a.trace, ((int64_t)g * B + b) * (a.bt_stride * kPage) + pg * kPage + st_key, tile / D + st_key);
+      }
       const __amdgpu_buffer_rsrc_t rk = tile_rsrc<uint16_t, D>(kp + tile, valid);
       const __amdgpu_buffer_rsrc_t rv = tile_rsrc<uint16_t, D>(vp + tile, valid);
       kr = __builtin_amdgcn_raw_buffer_load_b128(rk, st_ld, 0, kPfLoadPolicy);

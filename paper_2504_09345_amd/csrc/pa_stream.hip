@@ -16,68 +16,42 @@
 //  * A (row, head) item that lies inside one range is finished in place.  An
 //    item cut by a range boundary leaves partial (o, m, l) records, at most
 //    two per workgroup ("head": the range starts inside the item, "tail": the
-//    item continues past the range).  The workgroup holding an item's first
-//    part merges the later ranges' records once their flags carry this
-//    call's token, in range order (deterministic, no float atomics): one
-//    launch per call.
+//    item continues past the range).  Each part counts its arrival at the
+//    item's counter once its record is stored; the last part to arrive merges
+//    every record in range order (deterministic, no float atomics, and no
+//    workgroup ever waits for another): one launch per call.
 //
 // Per workgroup: prefix sums of page counts over all rows (LDS), then a unit
 // table for its range (page id and flags per unit, LDS), then each wave runs
 // a ring of NBUF register tile buffers over the units, exactly as in the
 // split kernel's inner loop, with a workgroup barrier per unit to keep the
 // waves in step.
-#include "pa_stream_body.h"
+#include "pa_stream_kernel.h"
 
 namespace pa {
 
-template <typename T, int D, int S, int W, int NBUF, bool MF>
-__global__ __launch_bounds__(64 * W) void stream_kernel(StreamArgs a) {
-  __shared__ StreamSmem<W, MF> sm;
-  stream_body<T, D, S, W, NBUF, MF>(a, sm, blockIdx.x, gridDim.x);
-}
+// Kernels of the other (element type, head dim) combinations and the trace
+// instantiations are compiled in their own translation units.
+extern template const void* stream_pick<uint16_t, 64, false>(int, int);
+extern template const void* stream_pick<float, 128, false>(int, int);
+extern template const void* stream_pick<float, 64, false>(int, int);
+extern template const void* stream_pick<uint16_t, 128, true>(int, int);
+extern template const void* stream_pick<uint16_t, 64, true>(int, int);
+extern template const void* stream_pick<float, 128, true>(int, int);
+extern template const void* stream_pick<float, 64, true>(int, int);
+template const void* stream_pick<uint16_t, 128, false>(int, int);
 
-// ---- launchers -----------------------------------------------------------
-
-template <typename T, int D, int S, int W>
-static const void* stream_fn() {
-  constexpr bool mf = kStreamMfma && sizeof(T) == 2 && D == 128;
-  return reinterpret_cast<const void*>(&stream_kernel<T, D, S, W, kStreamRing, mf>);
-}
-
-template <typename T, int D, int S>
-static const void* pick_w(int W) {
-  switch (W) {
-    case 1: return stream_fn<T, D, S, 1>();
-    case 2: return stream_fn<T, D, S, 2>();
-    case 4: return stream_fn<T, D, S, 4>();
-    case 8: return stream_fn<T, D, S, 8>();
-  }
-  return nullptr;
-}
-
-template <typename T, int D>
-static const void* pick_s(int s, int W) {
-  switch (s) {
-    case 1: return pick_w<T, D, 1>(W);
-    case 2: return pick_w<T, D, 2>(W);
-    case 4: return pick_w<T, D, 4>(W);
-    case 6: return pick_w<T, D, 6>(W);
-    case 8: return pick_w<T, D, 8>(W);
-  }
-  return nullptr;
-}
-
-const void* stream_kernel_fn(int dtype, int D, int s, int W) {
-  if (dtype == 0 && D == 128) return pick_s<uint16_t, 128>(s, W);
-  if (dtype == 0 && D == 64) return pick_s<uint16_t, 64>(s, W);
-  if (dtype == 1 && D == 128) return pick_s<float, 128>(s, W);
-  if (dtype == 1 && D == 64) return pick_s<float, 64>(s, W);
+static const void* stream_kernel_fn(int dtype, int D, int s, int W, bool trace) {
+  if (dtype == 0 && D == 128) return trace ? stream_pick<uint16_t, 128, true>(s, W) : stream_pick<uint16_t, 128, false>(s, W);
+  if (dtype == 0 && D == 64) return trace ? stream_pick<uint16_t, 64, true>(s, W) : stream_pick<uint16_t, 64, false>(s, W);
+  if (dtype == 1 && D == 128) return trace ? stream_pick<float, 128, true>(s, W) : stream_pick<float, 128, false>(s, W);
+  if (dtype == 1 && D == 64) return trace ? stream_pick<float, 64, true>(s, W) : stream_pick<float, 64, false>(s, W);
   return nullptr;
 }
 
 hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, int G, hipStream_t st,
                          KernelEvents ev) {
-  const void* fn = stream_kernel_fn(dtype, D, s, W);
+  const void* fn = stream_kernel_fn(dtype, D, s, W, a.trace != nullptr);
   if (fn == nullptr || G <= 0) return hipErrorInvalidValue;
   void* args[] = {const_cast<StreamArgs*>(&a)};
   hipError_t e = hipExtLaunchKernel(fn, dim3(G), dim3(64 * W), args, 0, st, ev.start, ev.stop, 0);
@@ -85,9 +59,8 @@ hipError_t launch_stream(int dtype, int D, int s, int W, const StreamArgs& a, in
   return hipGetLastError();
 }
 
-
 int stream_occupancy(int dtype, int D, int s, int W) {
-  const void* fn = stream_kernel_fn(dtype, D, s, W);
+  const void* fn = stream_kernel_fn(dtype, D, s, W, false);
   if (fn == nullptr) return 0;
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, 64 * W, 0) != hipSuccess) return 0;

@@ -20,7 +20,10 @@ __device__ __forceinline__ int info_row(int i) { return (int)((unsigned)i >> 13)
 // Merge the partial records of item (row r, KV head g) held by ranges
 // wg_first .. wg_last (record slot 1 of wg_first, slot 0 of the others; empty
 // ranges wrote nothing) and write the output row: one wave, E elements per
-// lane, records merged in range order.
+// lane, records merged in range order.  Every part of the item stores its
+// record before it counts its arrival, and whichever part arrives last runs
+// this merge over all the records, so the result does not depend on which
+// range merges.
 template <typename T, int D, int S, int W>
 __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64_t G, int64_t wg_first,
                                            int64_t wg_last, int w, int lane, T* out) {
@@ -44,14 +47,24 @@ __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64
     float c[S];
 #pragma unroll
     for (int j = 0; j < S; ++j) {
-      c[j] = fast_exp2(load_dev(a.ws_ml + slot * S * 2 + j * 2) - M[j]);
-      L[j] = fmaf(load_dev(a.ws_ml + slot * S * 2 + j * 2 + 1), c[j], L[j]);
+      float m, l;
+      load_dev2(a.ws_ml + slot * S * 2 + j * 2, m, l);
+      c[j] = fast_exp2(m - M[j]);
+      L[j] = fmaf(l, c[j], L[j]);
     }
     const float* o = a.ws_o + slot * S * D;
+    float v[E];
+    if constexpr (E % 2 == 0) {
+#pragma unroll
+      for (int e = 0; e < E; e += 2) load_dev2(o + lane * E + e, v[e], v[e + 1]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < E; ++e) v[e] = load_dev(o + lane * E + e);
+    }
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int idx = lane * E + e;
-      acc[e] = fmaf(load_dev(o + idx), c[idx / D], acc[e]);
+      acc[e] = fmaf(v[e], c[idx / D], acc[e]);
     }
   }
 #pragma unroll
@@ -60,6 +73,28 @@ __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64
     store_out<T>(out + idx, acc[e] / L[idx / D]);
   }
 }
+
+// Count one part's arrival at an item's counter and return the parts counted
+// so far, this one included.  The counter's upper 48 bits carry the call's
+// token and its lower 16 bits the count: a counter left by an earlier call
+// (or found in a fresh workspace) holds another token and starts over at 1.
+// The compare-and-swap only repeats when another part of the same item
+// changed the counter in between, so the loop ends after at most as many
+// rounds as the item has parts; nothing here waits for another workgroup.
+__device__ __forceinline__ int arrive_count(unsigned long long* ctr, unsigned long long token) {
+  const unsigned long long tag = (token & 0xffffffffffffull) << 16;
+  unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (;;) {
+    const unsigned long long base = (old & ~0xffffull) == tag ? old : tag;
+    if (__hip_atomic_compare_exchange_strong(ctr, &old, base + 1, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT))
+      return (int)((base + 1) & 0xffffull);
+  }
+}
+
+// Range (of G equal ranges over U units) that holds unit e: the largest x
+// with floor(U x / G) <= e.
+__device__ __forceinline__ int64_t range_of(int64_t e, int64_t U, int64_t G) { return ((e + 1) * G - 1) / U; }
 
 // Sequence of unit u: the largest r with nb * cum[r] <= u (a non-empty one).
 __device__ __forceinline__ int info_row_seq(const int32_t* cum, int R, int nb, int64_t u) {
@@ -87,7 +122,9 @@ struct StreamSmem {
 constexpr uint8_t kRowZeros = 0x20, kRowNaN = 0x40;
 
 // The stream-K decode workgroup `bid` of a grid of G (see pa_stream.hip).
-template <typename T, int D, int S, int W, int NBUF, bool MF>
+// TR: gather-trace instantiation (records every loaded token's pool row in
+// a.trace besides computing the attention).
+template <typename T, int D, int S, int W, int NBUF, bool MF, bool TR = false>
 __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, MF>& sm, int bid, int G_) {
   using Sh = DecodeShape<T, D, S>;
   constexpr int NT = 64 * W;
@@ -177,21 +214,53 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
       const int info = __builtin_amdgcn_readfirstlane(s_info[k]);
       off = tile_offset(page, info_hb(info) * W + w, a.H_kv, D);
       valid = info_valid(info);
+      if constexpr (TR) {
+        // (sequence, head block, page) of the unit, from the unit's index
+        const int r = info_row_seq(s_cum, R, a.nb, u0 + k);
+        const int np = s_cum[r + 1] - s_cum[r];
+        const int rem = (int)(u0 + k - (int64_t)a.nb * s_cum[r]);
+        const int hb = rem / np, p = rem - hb * np;
+        if (lane < valid)
+          trace_put(a.trace, ((int64_t)(hb * W + w) * R + r) * (a.bt_stride * kPage) + p * kPage + lane,
+                    off / D + lane);
+      }
     }
     issue_tile<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), tile_rsrc<T, D>(vp + off, valid), lane_off, kr, vr);
+  };
+
+  // Items cut by range boundaries.  Every part (the item's first part ends
+  // its range; a later part starts one) stores its partial record, then
+  // counts its arrival at the item's counter; the part that arrives last
+  // merges all the records in range order and writes the output.  Nothing
+  // waits on another workgroup, so the result and the kernel's completion do
+  // not depend on how many workgroups are resident or in which order they
+  // run.  Records travel through device-coherent stores and loads; a part
+  // counts itself only once its record stores have completed.
+  auto arrive = [&](int64_t x0, int64_t x1, int qrow, int g) {
+    int got = 0;
+    if (lane == 0) got = arrive_count(a.ws_flag + x0 * W + w, a.token);
+    got = __builtin_amdgcn_readfirstlane(got);
+    int parts = 0;
+    for (int64_t x = x0; x <= x1; ++x) parts += U * x / G != U * (x + 1) / G ? 1 : 0;
+    if (got == parts) {
+      T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)qrow * a.H_q + (int64_t)g * S) * D;
+      merge_item<T, D, S, W>(a, U, G, x0, x1, w, lane, outp);
+    }
   };
 
   u32x4 kr[NBUF][Sh::NI], vr[NBUF][Sh::NI];
 #pragma unroll
   for (int u = 0; u + 1 < NBUF; ++u) issue(kr[u], vr[u], u);
-  // A head record written at unit k is published one unit later, once the
-  // loads issued after it are the only ones outstanding: waiting for the
-  // record stores then does not drain the tile ring (the vector-memory
-  // counter retires loads and stores in issue order).
+  // A part whose record is stored at unit k < n_units - 1 counts its arrival
+  // one unit later, once the loads issued after the record are the only ones
+  // outstanding: waiting for the record stores then does not drain the tile
+  // ring (the vector-memory counter retires loads and stores in issue order).
   constexpr int kRingLoads = 2 * Sh::NI;  // load instructions of one issue()
   constexpr int kWaitRing = (kRingLoads & 15) | (7 << 4) | (15 << 8) | ((kRingLoads >> 4) << 14);
   static_assert(kRingLoads < 64, "vmcnt range");
-  bool publish = false;
+  bool pending = false;  // (wave-uniform) an arrival to count at the next unit
+  int64_t pend_x0 = 0, pend_x1 = 0;
+  int pend_row = 0, pend_g = 0;
   for (int base = 0; base < n_units; base += NBUF) {
 #pragma unroll
     for (int u = 0; u < NBUF; ++u) {
@@ -224,11 +293,10 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
         }
       }
       issue(kr[(u + NBUF - 1) % NBUF], vr[(u + NBUF - 1) % NBUF], k + NBUF - 1);
-      if (publish) {  // workgroup-uniform
-        publish = false;
+      if (pending) {  // wave-uniform
+        pending = false;
         __builtin_amdgcn_s_waitcnt(kWaitRing);  // everything but the tile just issued
-        __syncthreads();
-        if (tid == 0) __hip_atomic_store(a.ws_flag + bid, a.token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        arrive(pend_x0, pend_x1, pend_row, pend_g);
       }
       if (k < n_units) {
         if constexpr (MF)
@@ -240,63 +308,30 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
           const int r = info_row(info);
           const int g = info_hb(info) * W + w;
           T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)r * a.H_q + (int64_t)g * S) * D;
-          const int64_t slot = ((int64_t)bid * 2 + (head_partial ? 0 : 1)) * W + w;
-          if constexpr (MF) {
-            if (!head_partial && !tail_partial)
+          if (!head_partial && !tail_partial) {  // the whole item in this range
+            if constexpr (MF)
               mfma::finish<S, T>(ms, lane, outp);
-            else if (head_partial)  // (the range holding the item's first part merges from registers)
-              mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
-          } else {
-            if (!head_partial && !tail_partial)
+            else
               finish_rows<T, D, S>(st, row, dl, outp);
+          } else {  // (workgroup-uniform)
+            const int64_t slot = ((int64_t)bid * 2 + (head_partial ? 0 : 1)) * W + w;
+            if constexpr (MF)
+              mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
             else
               partial_rows<T, D, S>(st, row, dl, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
-          }
-          // Items cut by range boundaries (the branches are workgroup-uniform).
-          // Records travel through device-coherent stores and loads.  A range
-          // holding a later part publishes its head record: each wave waits
-          // for its record stores to complete, the barrier gathers the waves,
-          // then thread 0 sets the range's flag to this call's token (at the
-          // next unit, see above, unless the range ends here).  The
-          // range holding the item's first part waits for the later ranges'
-          // flags, then merges in range order: from its registers and the later
-          // records (matrix-core fold), or from every record (VALU fold, which
-          // stores its own tail record first).
-          // A range only ever waits on higher ranges, and writes its head
-          // record before it waits, so the waits always end.
-          if (head_partial) {
-            if (k + 1 < n_units) {
-              publish = true;  // at the next unit
-            } else {
-              __builtin_amdgcn_s_waitcnt(0);
-              __syncthreads();
-              if (tid == 0) __hip_atomic_store(a.ws_flag + bid, a.token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-          } else if (tail_partial) {
+            // the item's first and last units, and the ranges holding them
             const int rr = info_row_seq(s_cum, R, a.nb, u0 + k);
             const int np = s_cum[rr + 1] - s_cum[rr];
-            const int64_t e_last = (int64_t)a.nb * s_cum[rr] + (int64_t)info_hb(info) * np + np - 1;
-            const int64_t wg_last = ((e_last + 1) * G - 1) / U;
-            if constexpr (!MF) __builtin_amdgcn_s_waitcnt(0);  // this range's own tail record is stored
-            __syncthreads();
-            if (tid == 0) {
-              for (int64_t x = bid + 1; x <= wg_last; ++x) {
-                if (U * x / G == U * (x + 1) / G) continue;  // empty range: nothing to wait for
-                while (__hip_atomic_load(a.ws_flag + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.token)
-                  __builtin_amdgcn_s_sleep(4);
-              }
-            }
-            __syncthreads();
-            if constexpr (MF) {
-              // own part in registers, later ranges' head records folded in range order
-              for (int64_t x = bid + 1; x <= wg_last; ++x) {
-                if (U * x / G == U * (x + 1) / G) continue;
-                const int64_t sx = (x * 2) * W + w;
-                mfma::merge_record<S>(ms, a.ws_o + sx * S * D, a.ws_ml + sx * S * 2, lane);
-              }
-              mfma::finish<S, T>(ms, lane, outp);
+            const int64_t e_first = (int64_t)a.nb * s_cum[rr] + (int64_t)info_hb(info) * np;
+            pend_x0 = range_of(e_first, U, G);
+            pend_x1 = range_of(e_first + np - 1, U, G);
+            pend_row = r;
+            pend_g = g;
+            if (k + 1 < n_units) {
+              pending = true;  // counted at the next unit
             } else {
-              merge_item<T, D, S, W>(a, U, G, bid, wg_last, w, lane, outp);
+              __builtin_amdgcn_s_waitcnt(0);  // the record stores have completed
+              arrive(pend_x0, pend_x1, pend_row, pend_g);
             }
           }
         }

@@ -76,9 +76,10 @@ def _align(x):
     return (x + 255) // 256 * 256
 
 
-def _stream_ws(B, H_q, D):
+def _stream_ws(B, H_q, D, W=8):
     recs = 1024 * 2 * H_q  # (workgroup, slot) x (waves x group) = all query heads of a head block
-    return _align(recs * D * 4) + _align(recs * 2 * 4) + _align(1024 * 8)  # records, (m, l), range flags
+    # records, (m, l), arrival counters per (first range, wave)
+    return _align(recs * D * 4) + _align(recs * 2 * 4) + _align(1024 * W * 8)
 
 
 def _split_ws(rows, H_q, D, max_ctx, pps):
@@ -200,16 +201,62 @@ def test_paged_attn_varlen_validation(case):
 def test_gather_trace_validation():
     import ctypes
     lib = pb.load()
-    d = dims()
-    assert lib.pa_gather_trace(None, FAKE, FAKE, ctypes.byref(d), FAKE, None) == pb.PA_EINVAL
-    d2 = dims(page_size=8)
-    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, ctypes.byref(d2), FAKE, None) == pb.PA_ENOTSUP
-    d3 = dims(max_pages_per_seq=3)
-    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, ctypes.byref(d3), FAKE, None) == pb.PA_EINVAL
-    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, None, FAKE, None) == pb.PA_EINVAL
+
+    def call(d, q=FAKE, qsl=None, rows=FAKE, ws_bytes=None, scale=0.088):
+        ws_bytes = pb.pa_workspace_size(d) if ws_bytes is None else ws_bytes
+        return lib.pa_gather_trace(q, FAKE, FAKE, FAKE, FAKE, qsl, scale, FAKE, ctypes.byref(d), FAKE,
+                                   ws_bytes, rows, None)
+    assert call(dims(), q=None) == pb.PA_EINVAL
+    assert call(dims(), rows=None) == pb.PA_EINVAL
+    assert call(dims(), scale=0.0) == pb.PA_EINVAL
+    assert call(dims(), ws_bytes=100) == pb.PA_ENOSPC
+    assert call(dims(page_size=8), ws_bytes=0) == pb.PA_ENOTSUP
+    assert call(dims(max_pages_per_seq=3), ws_bytes=0) == pb.PA_EINVAL
+    assert lib.pa_gather_trace(FAKE, FAKE, FAKE, FAKE, FAKE, None, 0.088, FAKE, None, FAKE, 0, FAKE,
+                               None) == pb.PA_EINVAL
+    # varlen trace: the varlen call's validation
+    vd = dims(num_seqs=520, num_q_rows=4608, max_q_len=0, max_context_len=4096, max_pages_per_seq=256)
+    assert call(vd, qsl=FAKE, ws_bytes=1 << 40) == pb.PA_EINVAL
     # nothing to trace: success without touching the pointers
     d4 = dims(num_seqs=0)
-    assert lib.pa_gather_trace(None, None, None, ctypes.byref(d4), None, None) == pb.PA_OK
+    assert lib.pa_gather_trace(None, None, None, None, None, None, 0.088, None, ctypes.byref(d4), None, 0,
+                               None, None) == pb.PA_OK
+
+
+@host_only
+@pytest.mark.parametrize("dtype,D", [(pb.PA_FP32, 128), (pb.PA_BF16, 64), (pb.PA_FP32, 64)])
+def test_varlen_all_single_rows_fit_the_sized_workspace(dtype, D):
+    """A varlen call whose rows are all decode rows (every L_b = 1) is planned
+    like the decode call: the stream kernel takes every row, so no split-K
+    partials are reserved, also where the chunk kernel does not apply (fp32,
+    head_dim 64) and contexts exceed one split granule.  Validation must pass
+    with exactly pa_workspace_size() bytes (it then reaches the first HIP call,
+    which fails where no GPU is visible)."""
+    import ctypes
+    d = dims(dtype=dtype, head_dim=D, num_seqs=64, num_q_rows=64, max_q_len=1, max_context_len=4096,
+             max_pages_per_seq=256)
+    need = pb.pa_workspace_size(d)
+    dec = dims(dtype=dtype, head_dim=D, num_seqs=64, max_context_len=4096, max_pages_per_seq=256)
+    assert need == pb.pa_workspace_size(dec)
+    rc = pb.load().paged_attn_varlen(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0.088, FAKE, ctypes.byref(d),
+                                     FAKE, need, None, None)
+    assert rc == pb.PA_EHIP
+    # the same call with chunk rows reserves split-K partials (fp32 / D 64
+    # chunk rows take the per-row kernel)
+    d.num_q_rows, d.max_q_len = 128, 2
+    assert pb.pa_workspace_size(d) > need
+
+
+@host_only
+def test_read_probe_validation():
+    lib = pb.load()
+    assert lib.pa_read_probe(None, 4096, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, 1, 1, 1, None, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 1000, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 0, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, -1, 1, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, 1, 0, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, 1, 70000, 1, FAKE, None) == pb.PA_EINVAL
 
 
 @host_only

@@ -2,7 +2,8 @@
 same seeded inputs, element by element, plus the structural checks (bit-exact
 block-table gather, split-size invariance, determinism, poisoned pools, edge
 cases).  Full-size workloads are checked on sampled sequences in the launch
-configuration the benchmark times."""
+configuration the benchmark times.  The kernels' own block-table gather is
+checked bit for bit in test_gpu_gather.py."""
 import functools
 
 import numpy as np
@@ -121,28 +122,6 @@ def test_context_beyond_declared_bound_is_flagged():
     assert_parity(got[:3], run_oracle(b)[:3])
 
 
-def test_gather_trace_bit_exact():
-    torch = _torch()
-    for name, seed in (("tiny", 0), ("mixtral-256", 1)):
-        announce(f"gather trace {name}")
-        b = W.generate(name, seed=seed) if name == "tiny" else _full(name, seed)
-        bt = torch.from_numpy(b.block_table).cuda()
-        cl = torch.from_numpy(b.context_lens).cuda()
-        starts = np.zeros(b.num_seqs, np.int64)
-        starts[1:] = np.cumsum(b.context_lens.astype(np.int64))[:-1]
-        rs = torch.from_numpy(starts).cuda()
-        total = int(b.context_lens.sum())
-        rows = torch.full((total,), -7, dtype=torch.int64, device="cuda")
-        dims = pb.PaDims(num_seqs=b.num_seqs, num_q_heads=1, num_kv_heads=1, head_dim=128,
-                         page_size=16, num_pages=b.num_pages, max_pages_per_seq=b.max_pages_per_seq,
-                         max_context_len=int(b.context_lens.max()), pages_per_split=0, dtype=0,
-                         num_q_rows=0, max_q_len=0)
-        pb.pa_gather_trace(bt, cl, rs, dims, rows)
-        torch.cuda.synchronize()
-        ref = oracle.gather_indices(b.block_table, b.context_lens, 16, b.num_pages)
-        assert np.array_equal(rows.cpu().numpy(), ref)
-
-
 # --- varlen: causal prefill chunks sharing the launch with decode rows ------
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
@@ -181,8 +160,8 @@ def _sample(batch, n, seed):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("name,seed,n", [("mixtral-256", 1, 48), ("long-ctx-64", 2, 6),
-                                         ("dbrx-512", 3, 48)])
+@pytest.mark.parametrize("name,seed,n", [("mixtral-256", 1, 64), ("long-ctx-64", 2, 16),
+                                         ("dbrx-512", 3, 64)])
 def test_full_size_decode_sampled(name, seed, n):
     announce(f"full {name} seed={seed}: generate")
     b = _full(name, seed)
@@ -200,7 +179,8 @@ def test_full_size_mixed_sampled():
     b = _full("mixed", 4)
     announce(f"full mixed: gpu run rows={b.num_q_rows}")
     got = run_gpu(b)
-    seqs = [0, 5] + list(range(8, 520, 16))
+    # all 8 prefill chunks (4,096 rows) and every eighth decode row (64)
+    seqs = list(range(8)) + list(range(8, 520, 8))
     sb, rows = sub_batch(b, seqs)
     ref = run_oracle(sb)
     assert_parity(got[rows], ref, strict=False, what="mixed")
