@@ -164,6 +164,33 @@ int paged_attn_varlen(const void *q, const void *k_pages, const void *v_pages,
                       const pa_dims_t *dims, void *workspace, size_t workspace_bytes,
                       hipStream_t stream, const pa_timing_t *timing);
 
+/* No-allocation variant of paged_attn_varlen, for callers that cannot
+ * allocate device memory or pass a workspace: code recorded under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, layouts, results and errors as paged_attn_varlen, without the
+ * workspace: the partial records and arrival counters live in a fixed
+ * 32 MiB array of device memory inside the library (one per GPU, held until
+ * the process ends; its address is taken on the first call on each device).
+ * The call allocates nothing.
+ *   - A call that needs more than the 32 MiB returns PA_ENOSPC and enqueues
+ *     nothing.  The stream-K decode rows need 66.5 KiB per workgroup of the
+ *     grid at s = 8 (33 KiB at s = 4, 208 workgroups on MI355X: ~7 MB);
+ *     chunk rows that take the per-row split-K kernel (fp32, head_dim 64)
+ *     need rows x H_q x splits x (D + 2) x 4 bytes.
+ *   - Every call on one GPU shares that GPU's array and leaves its contents
+ *     behind (the arrival counters are tagged per call, so nothing needs
+ *     clearing): calls that overlap in time on one GPU (other streams,
+ *     other threads) race on it and must be serialised by the caller.
+ *   - Decode-only callers pass query_start_loc = {0, 1, ..., num_seqs} with
+ *     num_q_rows = num_seqs and max_q_len = 1, which runs exactly the kernels
+ *     of paged_attn.
+ * Errors: as paged_attn_varlen; PA_EHIP also when the scratch's device
+ * address cannot be taken. */
+int paged_attn_varlen_noalloc(const void *q, const void *k_pages, const void *v_pages,
+                              const int32_t *block_table, const int32_t *context_lens,
+                              const int32_t *query_start_loc, float scale, void *out,
+                              const pa_dims_t *dims, hipStream_t stream, const pa_timing_t *timing);
+
 /* Block-table gather trace (Sec. 5.5 paging; Sec. 2 GQA): the same call as
  * paged_attn (query_start_loc == NULL) or paged_attn_varlen (otherwise), run
  * through instantiations of the very same kernels that also record, for every

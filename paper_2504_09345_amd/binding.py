@@ -20,7 +20,8 @@ PA_OK, PA_EINVAL, PA_ENOTSUP, PA_ENOSPC, PA_EHIP = 0, -1, -2, -3, -4
 PA_BF16, PA_FP32 = 0, 1
 PAGE_SIZE = 16
 
-EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "pa_gather_trace",
+EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "paged_attn_varlen_noalloc",
+            "pa_gather_trace",
             "pa_kv_append", "pa_schedule_step", "pa_perf_model", "pa_read_probe", "pa_strerror")
 
 
@@ -104,6 +105,8 @@ def load():
     lib.paged_attn.restype = ctypes.c_int
     lib.paged_attn_varlen.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, DP, P, SZ, P, TP]
     lib.paged_attn_varlen.restype = ctypes.c_int
+    lib.paged_attn_varlen_noalloc.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, DP, P, TP]
+    lib.paged_attn_varlen_noalloc.restype = ctypes.c_int
     lib.pa_gather_trace.argtypes = [P, P, P, P, P, P, ctypes.c_float, P, DP, P, SZ, P, P]
     lib.pa_gather_trace.restype = ctypes.c_int
     lib.pa_kv_append.argtypes = [P, P, P, P, P, P, P, DP, P]
@@ -218,6 +221,19 @@ def paged_attn_varlen(q, k_pages, v_pages, block_table, context_lens, query_star
                                   ctypes.byref(timing) if timing is not None else None)
     if check and rc != PA_OK:
         raise PagedAttnError("paged_attn_varlen", rc)
+    return rc
+
+
+def paged_attn_varlen_noalloc(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out,
+                              dims: PaDims, stream=None, timing: PaTiming | None = None, check=True) -> int:
+    """int paged_attn_varlen_noalloc(...): paged_attn_varlen with the library's
+    fixed device scratch in place of a workspace (allocates nothing)."""
+    rc = load().paged_attn_varlen_noalloc(_addr(q), _addr(k_pages), _addr(v_pages), _addr(block_table),
+                                          _addr(context_lens), _addr(query_start_loc), float(scale),
+                                          _addr(out), ctypes.byref(dims), _stream(stream),
+                                          ctypes.byref(timing) if timing is not None else None)
+    if check and rc != PA_OK:
+        raise PagedAttnError("paged_attn_varlen_noalloc", rc)
     return rc
 
 

@@ -9,6 +9,7 @@
 
 #include <atomic>
 #include <chrono>
+#include <mutex>
 
 #include "pa_kernels.h"
 #include "pa_sched.h"
@@ -130,10 +131,10 @@ int plan(const pa_dims_t* d, bool varlen, Plan* p) {
   return PA_OK;
 }
 
-// Tag of one call's range flags in the workspace: process-wide, never 0 and
-// never repeated, so flags left in a reused workspace by earlier calls (or
-// found in a fresh one) do not match.  This counter is the library's only
-// state; it does not influence any result.
+// Tag of one call's arrival counters in the workspace: process-wide, never 0
+// and never repeated, so counters left in a reused workspace by earlier calls
+// (or found in a fresh one) do not match.  This counter is the library's only
+// state besides the fixed scratch below; it does not influence any result.
 unsigned long long next_token() {
   static std::atomic<unsigned long long> counter{
       0x9e3779b97f4a7c15ull ^
@@ -142,8 +143,51 @@ unsigned long long next_token() {
   return t != 0 ? t : counter.fetch_add(1, std::memory_order_relaxed) + 1;
 }
 
+// Fixed device scratch of paged_attn_varlen_noalloc: the workspace of a call
+// made by a caller that cannot allocate.  Every GPU that runs the library
+// holds its own copy for the life of the process.  Host code never passes
+// the array's name to a kernel (on the host it is only a stand-in for the
+// symbol): it uses the device address that hipGetSymbolAddress returns, taken
+// once per device with that device current.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of the current device's scratch (set up on the first call
+// on that device).
+int scratch_address(void** addr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return PA_EHIP;
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return PA_EHIP;
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *addr = p;
+  return PA_OK;
+}
+
 void record(hipEvent_t ev, hipStream_t st) {
   if (ev != nullptr) (void)hipEventRecord(ev, st);
+}
+
+// Host checks of an attention call's arguments (after plan()).
+int check_args(const Plan& p, bool varlen, const void* q, const void* k_pages, const void* v_pages,
+               const int32_t* block_table, const int32_t* context_lens, const int32_t* query_start_loc,
+               float scale, const void* out) {
+  if (!isfinite(scale) || !(scale > 0.0f)) return PA_EINVAL;
+  if (p.rows > 0) {
+    if (!q || !k_pages || !v_pages || !block_table || !context_lens || !out) return PA_EINVAL;
+    if (varlen && !query_start_loc) return PA_EINVAL;
+  }
+  return PA_OK;
 }
 
 // One attention call.  trace: nullptr, or the gather trace's array (the
@@ -151,16 +195,17 @@ void record(hipEvent_t ev, hipStream_t st) {
 int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
         const int32_t* context_lens, const int32_t* query_start_loc, float scale, void* out,
         const pa_dims_t* dims, void* workspace, size_t workspace_bytes, hipStream_t stream,
-        const pa_timing_t* timing, bool varlen, int64_t* trace = nullptr) {
+        const pa_timing_t* timing, bool varlen, int64_t* trace = nullptr, bool fixed_scratch = false) {
   Plan p;
   int rc = plan(dims, varlen, &p);
   if (rc != PA_OK) return rc;
-  if (!isfinite(scale) || !(scale > 0.0f)) return PA_EINVAL;
-  if (p.rows > 0) {
-    if (!q || !k_pages || !v_pages || !block_table || !context_lens || !out) return PA_EINVAL;
-    if (varlen && !query_start_loc) return PA_EINVAL;
-  }
-  if (p.ws_bytes > 0 && (workspace == nullptr || workspace_bytes < p.ws_bytes)) return PA_ENOSPC;
+  rc = check_args(p, varlen, q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out);
+  if (rc != PA_OK) return rc;
+  // A caller's workspace must hold pa_workspace_size() bytes (sized for the
+  // largest grid); the fixed scratch of the no-allocation entry only needs
+  // what this call's grid uses (checked below, once the grid is known).
+  if (!fixed_scratch && p.ws_bytes > 0 && (workspace == nullptr || workspace_bytes < p.ws_bytes))
+    return PA_ENOSPC;
   if (p.rows > 0 && p.split == false && p.stream == false) return PA_ENOTSUP;
 
   const hipEvent_t ev_begin = timing ? timing->attn_begin : nullptr;
@@ -198,6 +243,13 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     if (g < p.g_min) g = p.g_min;
     if (g > pa::kStreamMaxGrid) g = pa::kStreamMaxGrid;
     G = (int)g;
+    // workspace layout of this call: records and counters of G ranges, then
+    // the split-K partials (a caller's workspace, sized for kStreamMaxGrid
+    // ranges, always holds it)
+    const size_t recs = (size_t)G * 2 * p.W * p.s;
+    p.st_o = align256(recs * (size_t)dims->head_dim * sizeof(float));
+    p.st_ml = align256(recs * 2 * sizeof(float));
+    p.st_cum = align256((size_t)G * p.W * sizeof(unsigned long long));
     sa.q = q;
     sa.k_pages = k_pages;
     sa.v_pages = v_pages;
@@ -218,6 +270,7 @@ int run(const void* q, const void* k_pages, const void* v_pages, const int32_t* 
     sa.nb = p.nb;
     sa.trace = trace;
   }
+  if (p.st_o + p.st_ml + p.st_cum + p.sp_o + p.sp_ml > workspace_bytes) return PA_ENOSPC;
   // Mixed batch: decode and prefill workgroups side by side in one launch,
   // unless the chunk rows outweigh the decode rows.  A decode row streams its
   // whole KV (HBM-bound); a chunk row costs about s/80 of that on the matrix
@@ -371,6 +424,25 @@ int paged_attn_varlen(const void* q, const void* k_pages, const void* v_pages,
              workspace, workspace_bytes, stream, timing, true);
 }
 
+int paged_attn_varlen_noalloc(const void* q, const void* k_pages, const void* v_pages,
+                              const int32_t* block_table, const int32_t* context_lens,
+                              const int32_t* query_start_loc, float scale, void* out,
+                              const pa_dims_t* dims, hipStream_t stream, const pa_timing_t* timing) {
+  Plan p;  // host validation before the first device call
+  int rc = plan(dims, true, &p);
+  if (rc != PA_OK) return rc;
+  rc = check_args(p, true, q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out);
+  if (rc != PA_OK) return rc;
+  if (p.rows == 0)
+    return run(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out, dims, nullptr, 0,
+               stream, timing, true);
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc != PA_OK) return rc;
+  return run(q, k_pages, v_pages, block_table, context_lens, query_start_loc, scale, out, dims, ws,
+             kScratchBytes, stream, timing, true, nullptr, true);
+}
+
 int pa_gather_trace(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
                     const int32_t* context_lens, const int32_t* query_start_loc, float scale, void* out,
                     const pa_dims_t* dims, void* workspace, size_t workspace_bytes, int64_t* rows_out,
@@ -480,7 +552,7 @@ const char* pa_strerror(int code) {
     case PA_OK: return "success";
     case PA_EINVAL: return "invalid argument (null pointer, negative or inconsistent size)";
     case PA_ENOTSUP: return "unsupported configuration (head_dim, page_size, dtype or GQA group size)";
-    case PA_ENOSPC: return "workspace smaller than pa_workspace_size()";
+    case PA_ENOSPC: return "workspace smaller than pa_workspace_size() (or the call needs more than the no-allocation entry's fixed scratch)";
     case PA_EHIP: return "HIP kernel launch failed";
     default: return "unknown error code";
   }

@@ -248,6 +248,29 @@ def test_varlen_all_single_rows_fit_the_sized_workspace(dtype, D):
 
 
 @host_only
+@pytest.mark.parametrize("case", ["null_q", "null_qsl", "nan_scale", "bad_group", "rows_without_qlen"])
+def test_noalloc_validation(case):
+    """The no-allocation entry validates like paged_attn_varlen on the host,
+    before it touches a device."""
+    import ctypes
+    d = dims(num_seqs=520, num_q_rows=4608, max_q_len=512, max_context_len=4096, max_pages_per_seq=256)
+    q, qsl, scale = FAKE, FAKE, 0.088
+    if case == "null_q":
+        q = None
+    elif case == "null_qsl":
+        qsl = None
+    elif case == "nan_scale":
+        scale = float("nan")
+    elif case == "bad_group":
+        d.num_q_heads = 20
+    elif case == "rows_without_qlen":
+        d.max_q_len = 0
+    rc = pb.load().paged_attn_varlen_noalloc(q, FAKE, FAKE, FAKE, FAKE, qsl, scale, FAKE, ctypes.byref(d),
+                                             None, None)
+    assert rc == pb.PA_EINVAL
+
+
+@host_only
 def test_read_probe_validation():
     lib = pb.load()
     assert lib.pa_read_probe(None, 4096, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
