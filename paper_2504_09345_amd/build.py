@@ -22,12 +22,25 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
 
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
+# Host-code sanitizer build (device code unchanged): every host pass gets
+# AddressSanitizer and UndefinedBehaviorSanitizer, so the planning and
+# validation of the C ABI can run under them in the CPU test suites
+# (PAGEDATTN_LIB=<this path>, with clang's ASan runtime preloaded).
+LIB_ASAN = os.path.join(OUT_DIR, "libpagedattn_asan.so")
+SAN = ["-fsanitize=address", "-fsanitize=undefined"]
+SAN_HIP = [f for s in SAN for f in ("-Xarch_host", s)] + [
+    "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
 
-def _compile(src, obj, verbose):
+
+def _compile(src, obj, verbose, sanitize=False):
     if src.endswith(".cpp"):
-        cmd = ["g++", *HOST_FLAGS, "-c", src, "-o", obj]
+        if sanitize:  # clang's sanitizer runtime is the one loaded: compile with clang too
+            cmd = [os.path.join(os.path.dirname(HIPCC), "amdclang++"), *HOST_FLAGS, *SAN,
+                   "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-g", "-c", src, "-o", obj]
+        else:
+            cmd = ["g++", *HOST_FLAGS, "-c", src, "-o", obj]
     else:
-        cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+        cmd = [HIPCC, *FLAGS, *(SAN_HIP if sanitize else []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -39,22 +52,25 @@ def _compile(src, obj, verbose):
         print(err)
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, sanitize: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
+    out = LIB_ASAN if sanitize else LIB
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
-    objs = [os.path.join(OUT_DIR, os.path.splitext(os.path.basename(s))[0] + ".o") for s in srcs]
+    tag = "_asan" if sanitize else ""
+    objs = [os.path.join(OUT_DIR, os.path.splitext(os.path.basename(s))[0] + tag + ".o") for s in srcs]
     with ThreadPoolExecutor(min(8, len(srcs))) as ex:
-        list(ex.map(lambda so: _compile(so[0], so[1], verbose), zip(srcs, objs)))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+        list(ex.map(lambda so: _compile(so[0], so[1], verbose, sanitize), zip(srcs, objs)))
+    tmp = out + ".tmp"
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *(SAN_HIP if sanitize else []), "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     for o in objs:
         os.remove(o)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, sanitize="--sanitize-host" in sys.argv))
