@@ -32,7 +32,7 @@ SAN_HIP = [f for s in SAN for f in ("-Xarch_host", s)] + [
     "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
 
 
-def _compile(src, obj, verbose, sanitize=False):
+def _compile(src, obj, verbose, sanitize=False, defines=()):
     if src.endswith(".cpp"):
         if sanitize:  # clang's sanitizer runtime is the one loaded: compile with clang too
             cmd = [os.path.join(os.path.dirname(HIPCC), "amdclang++"), *HOST_FLAGS, *SAN,
@@ -40,7 +40,7 @@ def _compile(src, obj, verbose, sanitize=False):
         else:
             cmd = ["g++", *HOST_FLAGS, "-c", src, "-o", obj]
     else:
-        cmd = [HIPCC, *FLAGS, *(SAN_HIP if sanitize else []), "-c", src, "-o", obj]
+        cmd = [HIPCC, *FLAGS, *(SAN_HIP if sanitize else []), *[f"-D{d}" for d in defines], "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -52,14 +52,18 @@ def _compile(src, obj, verbose, sanitize=False):
         print(err)
 
 
-def build(verbose: bool = False, sanitize: bool = False) -> str:
+def build(verbose: bool = False, sanitize: bool = False, defines=(), out: str | None = None) -> str:
+    """Build the library.  defines: extra NAME=VALUE macros for the HIP
+    sources (tuning switches such as PA_STREAM_MFMA=0, the VALU fold of the
+    decode kernel); out: another output path for such a variant (load it with
+    PAGEDATTN_LIB=<path>)."""
     os.makedirs(OUT_DIR, exist_ok=True)
-    out = LIB_ASAN if sanitize else LIB
+    out = out or (LIB_ASAN if sanitize else LIB)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
-    tag = "_asan" if sanitize else ""
+    tag = "_asan" if sanitize else ("_" + os.path.splitext(os.path.basename(out))[0] if out != LIB else "")
     objs = [os.path.join(OUT_DIR, os.path.splitext(os.path.basename(s))[0] + tag + ".o") for s in srcs]
     with ThreadPoolExecutor(min(8, len(srcs))) as ex:
-        list(ex.map(lambda so: _compile(so[0], so[1], verbose, sanitize), zip(srcs, objs)))
+        list(ex.map(lambda so: _compile(so[0], so[1], verbose, sanitize, defines), zip(srcs, objs)))
     tmp = out + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *(SAN_HIP if sanitize else []), "-o", tmp, *objs]
     if verbose:
@@ -72,5 +76,11 @@ def build(verbose: bool = False, sanitize: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    import sys
-    print(build(verbose=True, sanitize="--sanitize-host" in sys.argv))
+    import argparse
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--sanitize-host", action="store_true")
+    ap.add_argument("--define", action="append", default=[], help="NAME=VALUE macro for the HIP sources")
+    ap.add_argument("--out", default=None, help="output path of a variant build")
+    a = ap.parse_args()
+    print(build(verbose=True, sanitize=a.sanitize_host, defines=a.define,
+                out=os.path.abspath(a.out) if a.out else None))
