@@ -225,8 +225,14 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hbm-probe", action="store_true",
                     help="also time the library's read-stream probe (pa_read_probe: the decode "
-                         "kernels' load pattern, sequential and random pages) over a 4 GiB buffer: "
-                         "the access pattern's ceiling, context for the roofline")
+                         "kernels' load pattern, sequential and random pages, 8 or 4 waves per "
+                         "workgroup) over a 4 GiB buffer: the access pattern's ceiling, context for "
+                         "the roofline")
+    ap.add_argument("--issue-probe", action="store_true",
+                    help="also time the library's issue-overlap probe (pa_issue_probe: bf16 matrix "
+                         "products beside independent FMAs or exponentials, in one wave or split "
+                         "across waves): how much vector work hides under the matrix cores, context "
+                         "for the prefill kernel's step time (adds an issue_probe object)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB before timing "
                          "(a known-size kernel for scaling profiler byte counters)")
@@ -419,6 +425,8 @@ def main():
         res["scheduler"], sched_replay = _sched_bench(torch, batch, K, args.seed)
     if args.hbm_probe:
         res["hbm_probe"] = _hbm_probe(torch)
+    if args.issue_probe:
+        res["issue_probe"] = _issue_probe(torch)
     if args.perf_model:
         res["perf_model"] = _perf_model_leg(torch, achieved * 1e9)
     if not args.no_cpu_baseline:
@@ -502,11 +510,13 @@ def _hbm_probe(torch, gib=4, reps=10):
     GPU: the library's probe kernel (pa_read_probe) reads a `gib` GiB buffer
     (16x the last-level cache, so every launch streams from HBM) in 4 KiB
     slices with the decode kernels' loads, on the decode kernel's grid (13/16
-    of the CUs) and on all CUs: sequentially; as randomly placed 32 KiB
-    chunks (one page of 8 KV heads, as the stream-K kernel reads them) with
-    the non-temporal policy the kernels use and with the default policy; and
-    as randomly placed 4 KiB tiles.  Events over `reps` back-to-back launches
-    after a warm-up."""
+    of the CUs) and on all CUs, with 8 waves per workgroup (the decode
+    kernel's) keeping two slices or one in flight, and with 4 waves keeping
+    two (the in-flight bytes of 8 waves keeping one): sequentially; as randomly
+    placed 32 KiB chunks (one page of 8 KV heads, as the stream-K kernel reads
+    them) with the non-temporal policy the kernels use and with the default
+    policy; and as randomly placed 4 KiB tiles.  Events over `reps`
+    back-to-back launches after a warm-up."""
     n = gib * (1 << 30)
     buf = torch.empty(n, dtype=torch.uint8, device="cuda")
     buf.fill_(1)
@@ -526,24 +536,80 @@ def _hbm_probe(torch, gib=4, reps=10):
             assert o.max() + chunk <= n  # every chunk inside the buffer
             offs = torch.from_numpy(o).cuda()
         row = {}
-        for gname, grid in grids.items():
-            for _ in range(2):
-                pb.pa_read_probe(buf, chunk, offs, n_chunks, grid, nt, sink)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(reps):
-                pb.pa_read_probe(buf, chunk, offs, n_chunks, grid, nt, sink)
-            e1.record()
-            torch.cuda.synchronize()
-            t = e0.elapsed_time(e1) / 1e3 / reps
-            row[gname] = {"grid": grid, "gb_per_s": round(n / t / 1e9, 1),
-                          "frac_of_hbm_peak": round(n / t / 1e9 / HBM_PEAK_GBPS, 4)}
+        for waves, depth in ((8, 2), (8, 1), (4, 2)):
+            for gname, grid in grids.items():
+                for _ in range(2):
+                    pb.pa_read_probe(buf, chunk, offs, n_chunks, grid, waves, depth, nt, sink)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    pb.pa_read_probe(buf, chunk, offs, n_chunks, grid, waves, depth, nt, sink)
+                e1.record()
+                torch.cuda.synchronize()
+                t = e0.elapsed_time(e1) / 1e3 / reps
+                row[f"{gname}_{waves}w_d{depth}"] = {
+                    "grid": grid, "waves": waves, "slices_in_flight_per_wave": depth,
+                    "gb_per_s": round(n / t / 1e9, 1), "frac_of_hbm_peak": round(n / t / 1e9 / HBM_PEAK_GBPS, 4)}
         out[name] = row
         del offs
     del buf, sink
-    out["note"] = (f"pa_read_probe over a {gib} GiB buffer, 4 KiB slices, 8 waves per workgroup, "
-                   f"{reps} launches each: the access pattern's ceiling, context for the roofline")
+    out["note"] = (f"pa_read_probe over a {gib} GiB buffer, 4 KiB slices, 8 or 4 waves per workgroup with "
+                   f"1 or 2 slices in flight per wave, {reps} launches each: the access pattern's ceiling, "
+                   f"context for the roofline")
+    return out
+
+
+def _issue_probe(torch, iters=4000, grid=256):
+    """How much vector-ALU work hides under the matrix products on this GPU:
+    the library's probe kernel (pa_issue_probe) on `grid` workgroups, four
+    independent bf16 products per iteration, each followed by n independent
+    vector instructions.  Each case is one launch of `iters` iterations after
+    a warm-up launch; it reports the median over waves of the loop's
+    shader-clock cycles per iteration (s_memtime, read by the kernel), and for
+    the interleaved and split cases the cycles hidden: products alone + vector
+    work alone - both together.  The clock the counter runs at follows from
+    the launch's event time and is reported beside it."""
+    sink = torch.empty(grid * 512, dtype=torch.float32, device="cuda")
+    cyc = torch.zeros(grid * 8, dtype=torch.int64, device="cuda")
+    clocks = []
+
+    def run(waves, big, nv, exp2, mode):
+        pb.pa_issue_probe(grid, waves, 10, big, nv, exp2, mode, sink)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        pb.pa_issue_probe(grid, waves, iters, big, nv, exp2, mode, sink, cyc)
+        e1.record()
+        torch.cuda.synchronize()
+        c = cyc[:grid * waves].cpu().numpy().astype(np.float64)
+        if mode == 3:  # the longer of the two halves sets the pace
+            c = np.maximum(c.reshape(grid, waves)[:, :waves // 2], c.reshape(grid, waves)[:, waves // 2:])
+        med = float(np.median(c))
+        clocks.append(med / (e0.elapsed_time(e1) * 1e3))  # counts per microsecond over the launch
+        return med / iters
+
+    out = {}
+    for big, name in ((0, "mfma_16x16x32_bf16"), (1, "mfma_32x32x16_bf16")):
+        alone = run(4, big, 0, 0, 1)
+        rows = {"products_alone": round(alone, 1)}
+        for exp2, vname, counts in ((0, "fma", (2, 3, 4, 6, 8, 16)), (1, "exp", (2, 4))):
+            for nv in counts:
+                v = run(4, big, nv, exp2, 2)
+                both = run(4, big, nv, exp2, 0)
+                rows[f"{nv}_{vname}"] = {"vector_alone": round(v, 1), "interleaved": round(both, 1),
+                                         "hidden": round(alone + v - both, 1)}
+        # the same work on two waves per SIMD: one issues the products, the other the FMAs
+        v8, split = run(4, big, 8, 0, 2), run(8, big, 8, 0, 3)
+        rows["split_8_fma"] = {"vector_alone": round(v8, 1), "split_waves": round(split, 1),
+                               "hidden": round(alone + v8 - split, 1)}
+        out[name] = rows
+    del sink, cyc
+    out["counter_mhz"] = {"min": round(min(clocks), 1), "median": round(float(np.median(clocks)), 1),
+                          "max": round(max(clocks), 1)}
+    out["note"] = (f"pa_issue_probe, {grid} workgroups of 4 waves (one per SIMD; the split cases 8), four "
+                   f"independent products per iteration, s_memtime cycles per iteration and wave (median over "
+                   f"waves), one launch of {iters} iterations per case")
     return out
 
 

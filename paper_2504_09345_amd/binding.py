@@ -22,7 +22,8 @@ PAGE_SIZE = 16
 
 EXPORTED = ("pa_workspace_size", "paged_attn", "paged_attn_varlen", "paged_attn_varlen_noalloc",
             "pa_gather_trace",
-            "pa_kv_append", "pa_schedule_step", "pa_perf_model", "pa_read_probe", "pa_strerror")
+            "pa_kv_append", "pa_schedule_step", "pa_perf_model", "pa_read_probe", "pa_issue_probe",
+            "pa_strerror")
 
 
 class PaDims(ctypes.Structure):
@@ -116,8 +117,11 @@ def load():
     lib.pa_schedule_step.restype = ctypes.c_int
     lib.pa_perf_model.argtypes = [ctypes.POINTER(PaPmInput), ctypes.POINTER(PaPmOutput)]
     lib.pa_perf_model.restype = ctypes.c_int
-    lib.pa_read_probe.argtypes = [P, ctypes.c_int64, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P]
+    lib.pa_read_probe.argtypes = [P, ctypes.c_int64, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_int32, P, P]
     lib.pa_read_probe.restype = ctypes.c_int
+    lib.pa_issue_probe.argtypes = [ctypes.c_int32] * 7 + [P, P, P]
+    lib.pa_issue_probe.restype = ctypes.c_int
     lib.pa_strerror.argtypes = [ctypes.c_int]
     lib.pa_strerror.restype = ctypes.c_char_p
     _lib = lib
@@ -276,14 +280,25 @@ def pa_schedule_step(state: PaSchedState, n_real, new_seq, new_prompt, new_fin, 
     return rc
 
 
-def pa_read_probe(buf, chunk_bytes, chunk_offsets, n_chunks, grid, non_temporal, sink, stream=None,
+def pa_read_probe(buf, chunk_bytes, chunk_offsets, n_chunks, grid, waves, depth, non_temporal, sink, stream=None,
                   check=True) -> int:
     """int pa_read_probe(...): read n_chunks chunks of buf with the decode
     kernels' load pattern (include/pa_probe.h)."""
     rc = load().pa_read_probe(_addr(buf), int(chunk_bytes), _addr(chunk_offsets), int(n_chunks), int(grid),
-                              int(non_temporal), _addr(sink), _stream(stream))
+                              int(waves), int(depth), int(non_temporal), _addr(sink), _stream(stream))
     if check and rc != PA_OK:
         raise PagedAttnError("pa_read_probe", rc)
+    return rc
+
+
+def pa_issue_probe(grid, waves, iters, big_mfma, valu_per_mfma, exp2, mode, sink, cycles=None, stream=None,
+                   check=True) -> int:
+    """int pa_issue_probe(...): matrix products beside vector work
+    (include/pa_probe.h); the caller times the launch."""
+    rc = load().pa_issue_probe(int(grid), int(waves), int(iters), int(big_mfma), int(valu_per_mfma), int(exp2),
+                               int(mode), _addr(sink), _addr(cycles), _stream(stream))
+    if check and rc != PA_OK:
+        raise PagedAttnError("pa_issue_probe", rc)
     return rc
 
 

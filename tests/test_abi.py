@@ -273,13 +273,18 @@ def test_noalloc_validation(case):
 @host_only
 def test_read_probe_validation():
     lib = pb.load()
-    assert lib.pa_read_probe(None, 4096, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
-    assert lib.pa_read_probe(FAKE, 4096, None, 1, 1, 1, None, None) == pb.PA_EINVAL
-    assert lib.pa_read_probe(FAKE, 1000, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
-    assert lib.pa_read_probe(FAKE, 0, None, 1, 1, 1, FAKE, None) == pb.PA_EINVAL
-    assert lib.pa_read_probe(FAKE, 4096, None, -1, 1, 1, FAKE, None) == pb.PA_EINVAL
-    assert lib.pa_read_probe(FAKE, 4096, None, 1, 0, 1, FAKE, None) == pb.PA_EINVAL
-    assert lib.pa_read_probe(FAKE, 4096, None, 1, 70000, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(None, 4096, None, 1, 1, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, 1, 1, 8, 2, 1, None, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 1000, None, 1, 1, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 0, None, 1, 1, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, -1, 1, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, 1, 0, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 4096, None, 1, 70000, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    for waves in (0, 2, 6, 16):
+        assert lib.pa_read_probe(FAKE, 4096, None, 1, 1, waves, 2, 1, FAKE, None) == pb.PA_EINVAL
+    assert lib.pa_read_probe(FAKE, 3 * 4096, None, 1, 1, 8, 2, 1, FAKE, None) == pb.PA_EINVAL
+    for depth in (0, 3, -1):
+        assert lib.pa_read_probe(FAKE, 4096, None, 1, 1, 8, depth, 1, FAKE, None) == pb.PA_EINVAL
 
 
 @host_only
@@ -387,3 +392,17 @@ def test_schedule_step_validation(case):
                               args["ns"], args["npr"], args["nf"], args["n_new"], args["qsl"],
                               args["fin"], args["info"], None)
     assert rc == expect
+
+
+def test_issue_probe_validation():
+    lib = pb.load()
+    ok = dict(grid=1, waves=4, iters=1, big=0, nv=2, exp2=0, mode=0, sink=FAKE)
+
+    def call(**kw):
+        a = {**ok, **kw}
+        return lib.pa_issue_probe(a["grid"], a["waves"], a["iters"], a["big"], a["nv"], a["exp2"], a["mode"],
+                                  a["sink"], None, None)
+
+    for bad in (dict(sink=None), dict(waves=3), dict(waves=16), dict(iters=0), dict(grid=0), dict(grid=70000),
+                dict(mode=4), dict(mode=-1), dict(mode=3, waves=1), dict(nv=5), dict(nv=17), dict(nv=-1)):
+        assert call(**bad) == pb.PA_EINVAL, bad
