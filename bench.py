@@ -239,8 +239,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the attention of one "
-                                   "GPU's share is measured; --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only: it measures the attention "
+                                   "of one GPU's share of a batch; --gpus must be 1"}))
         return 2
 
     import torch
