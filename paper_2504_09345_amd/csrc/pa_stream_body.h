@@ -78,12 +78,15 @@ __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64
 // so far, this one included.  The counter's upper 48 bits carry the call's
 // token and its lower 16 bits the count: a counter left by an earlier call
 // (or found in a fresh workspace) holds another token and starts over at 1.
-// The compare-and-swap only repeats when another part of the same item
-// changed the counter in between, so the loop ends after at most as many
-// rounds as the item has parts; nothing here waits for another workgroup.
-__device__ __forceinline__ int arrive_count(unsigned long long* ctr, unsigned long long token) {
+// The first compare-and-swap guesses that the other parts (parts - 1) have
+// all arrived, so the last part, which goes on to merge, usually needs one
+// round trip; a wrong guess returns the counter's value and the loop goes on
+// from it.  It only repeats when another part of the same item changed the
+// counter in between, so it ends after at most as many rounds as the item
+// has parts, plus the guess; nothing here waits for another workgroup.
+__device__ __forceinline__ int arrive_count(unsigned long long* ctr, unsigned long long token, int parts) {
   const unsigned long long tag = (token & 0xffffffffffffull) << 16;
-  unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  unsigned long long old = tag | (unsigned long long)(parts - 1);
   for (;;) {
     const unsigned long long base = (old & ~0xffffull) == tag ? old : tag;
     if (__hip_atomic_compare_exchange_strong(ctr, &old, base + 1, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
@@ -237,11 +240,11 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
   // run.  Records travel through device-coherent stores and loads; a part
   // counts itself only once its record stores have completed.
   auto arrive = [&](int64_t x0, int64_t x1, int qrow, int g) {
-    int got = 0;
-    if (lane == 0) got = arrive_count(a.ws_flag + x0 * W + w, a.token);
-    got = __builtin_amdgcn_readfirstlane(got);
     int parts = 0;
     for (int64_t x = x0; x <= x1; ++x) parts += U * x / G != U * (x + 1) / G ? 1 : 0;
+    int got = 0;
+    if (lane == 0) got = arrive_count(a.ws_flag + x0 * W + w, a.token, parts);
+    got = __builtin_amdgcn_readfirstlane(got);
     if (got == parts) {
       T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)qrow * a.H_q + (int64_t)g * S) * D;
       merge_item<T, D, S, W>(a, U, G, x0, x1, w, lane, outp);
