@@ -186,6 +186,20 @@ def test_full_size_mixed_sampled():
     assert_parity(got[rows], ref, strict=False, what="mixed")
 
 
+@pytest.mark.slow
+def test_full_size_prefill_alone():
+    """The 8 chunks of the mixed workload without decode rows, as the
+    benchmark's prefill workload times them: the chunked-prefill kernel alone
+    on every CU.  All 4,096 rows are compared."""
+    announce("full prefill-8x512 seed=1: generate")
+    b = _full("prefill-8x512", 1)
+    assert b.num_seqs == 8 and int(b.q_lens.min()) > 1  # no decode row: the prefill kernel alone
+    announce(f"full prefill-8x512: gpu run rows={b.num_q_rows}")
+    got = run_gpu(b)
+    ref = run_oracle(b)
+    assert_parity(got, ref, strict=False, what="prefill-8x512")
+
+
 # --- stream-K vs split-K ----------------------------------------------------
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
