@@ -80,6 +80,12 @@ constexpr int kStreamMaxGrid = 1024;    // persistent workgroups (partial-record
 #define PA_STREAM_RING 2
 #endif
 constexpr int kStreamRing = PA_STREAM_RING;
+#ifndef PA_STREAM_SPLIT_KV
+#define PA_STREAM_SPLIT_KV 1
+#endif
+// Matrix-core fold: load a unit's K and V tiles half a unit apart (one tile
+// of each in flight per wave) rather than through the NBUF ring.
+constexpr bool kStreamSplitKV = PA_STREAM_SPLIT_KV != 0;
 #ifndef PA_STREAM_MAX_WAVES
 #define PA_STREAM_MAX_WAVES 8
 #endif

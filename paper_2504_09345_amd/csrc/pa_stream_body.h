@@ -3,6 +3,8 @@
 // design).
 #pragma once
 
+#include <type_traits>
+
 #include "pa_device.h"
 #include "pa_kernels.h"
 #include "pa_tile.h"
@@ -209,26 +211,47 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
   auto& s_kv = sm.kv;
   bool head_partial = false;
 
-  auto issue = [&](u32x4 (&kr)[Sh::NI], u32x4 (&vr)[Sh::NI], int k) {
-    int valid = 0;
-    int64_t off = 0;
+  // Element offset and live tokens of unit k's tile for this wave (a null
+  // tile past the range); the trace instantiation records the tile's rows.
+  auto unit_tile = [&](int k, int64_t& off, int& valid, bool record) {
+    valid = 0;
+    off = 0;
     if (k < n_units) {
       const int page = __builtin_amdgcn_readfirstlane(s_page[k]);
       const int info = __builtin_amdgcn_readfirstlane(s_info[k]);
       off = tile_offset(page, info_hb(info) * W + w, a.H_kv, D);
       valid = info_valid(info);
       if constexpr (TR) {
-        // (sequence, head block, page) of the unit, from the unit's index
-        const int r = info_row_seq(s_cum, R, a.nb, u0 + k);
-        const int np = s_cum[r + 1] - s_cum[r];
-        const int rem = (int)(u0 + k - (int64_t)a.nb * s_cum[r]);
-        const int hb = rem / np, p = rem - hb * np;
-        if (lane < valid)
-          trace_put(a.trace, ((int64_t)(hb * W + w) * R + r) * (a.bt_stride * kPage) + p * kPage + lane,
-                    off / D + lane);
+        if (record) {
+          // (sequence, head block, page) of the unit, from the unit's index
+          const int r = info_row_seq(s_cum, R, a.nb, u0 + k);
+          const int np = s_cum[r + 1] - s_cum[r];
+          const int rem = (int)(u0 + k - (int64_t)a.nb * s_cum[r]);
+          const int hb = rem / np, p = rem - hb * np;
+          if (lane < valid)
+            trace_put(a.trace, ((int64_t)(hb * W + w) * R + r) * (a.bt_stride * kPage) + p * kPage + lane,
+                      off / D + lane);
+        }
       }
     }
+  };
+  auto issue = [&](u32x4 (&kr)[Sh::NI], u32x4 (&vr)[Sh::NI], int k) {
+    int64_t off;
+    int valid;
+    unit_tile(k, off, valid, true);
     issue_tile<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), tile_rsrc<T, D>(vp + off, valid), lane_off, kr, vr);
+  };
+  auto issue_k = [&](u32x4 (&kr)[Sh::NI], int k) {
+    int64_t off;
+    int valid;
+    unit_tile(k, off, valid, true);
+    issue_half<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), lane_off, kr);
+  };
+  auto issue_v = [&](u32x4 (&vr)[Sh::NI], int k) {
+    int64_t off;
+    int valid;
+    unit_tile(k, off, valid, false);
+    issue_half<Sh::NI>(tile_rsrc<T, D>(vp + off, valid), lane_off, vr);
   };
 
   // Items cut by range boundaries.  Every part (the item's first part ends
@@ -251,92 +274,179 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
     }
   };
 
-  u32x4 kr[NBUF][Sh::NI], vr[NBUF][Sh::NI];
-#pragma unroll
-  for (int u = 0; u + 1 < NBUF; ++u) issue(kr[u], vr[u], u);
   // A part whose record is stored at unit k < n_units - 1 counts its arrival
   // one unit later, once the loads issued after the record are the only ones
   // outstanding: waiting for the record stores then does not drain the tile
-  // ring (the vector-memory counter retires loads and stores in issue order).
-  constexpr int kRingLoads = 2 * Sh::NI;  // load instructions of one issue()
-  constexpr int kWaitRing = (kRingLoads & 15) | (7 << 4) | (15 << 8) | ((kRingLoads >> 4) << 14);
-  static_assert(kRingLoads < 64, "vmcnt range");
+  // loads in flight (the vector-memory counter retires loads and stores in
+  // issue order).
   bool pending = false;  // (wave-uniform) an arrival to count at the next unit
   int64_t pend_x0 = 0, pend_x1 = 0;
   int pend_row = 0, pend_g = 0;
-  for (int base = 0; base < n_units; base += NBUF) {
+
+  // Start of unit k, every wave in step (without the barrier the older wave
+  // of each SIMD runs ahead, waves 0..3 finish ~30% before waves 4..7, and
+  // those then stream the rest alone with half the loads in flight; in step,
+  // the W waves also issue the W adjacent head tiles of a page together).
+  // A new (row, head) item loads its queries.  Returns the unit's info word.
+  auto begin_unit = [&](int k) {
+    __syncthreads();
+    int info = 0;
+    if (k < n_units) {
+      info = __builtin_amdgcn_readfirstlane(s_info[k]);
+      if (info_start(info) || k == 0) {
+        head_partial = !info_start(info);
+        const int g = info_hb(info) * W + w;
+        const T* qg = qbase + ((int64_t)info_row(info) * a.H_q + (int64_t)g * S) * D;
+        if constexpr (MF) {
+          mfma::begin_item<S>(ms, reinterpret_cast<const uint16_t*>(qg), lane);
+        } else {
+          const T* qp = qg + dl * Sh::VEC;
 #pragma unroll
-    for (int u = 0; u < NBUF; ++u) {
-      // Lockstep: without a barrier the older wave of each SIMD runs ahead,
-      // waves 0..3 finish ~30% before waves 4..7, and those then stream the
-      // rest alone with half the loads in flight.  In step, the W waves also
-      // issue the W adjacent head tiles of a page together.
-      __syncthreads();
-      const int k = base + u;
-      int info = 0;
-      if (k < n_units) {
-        info = __builtin_amdgcn_readfirstlane(s_info[k]);
-        if (info_start(info) || k == 0) {  // a new (row, head) item: its queries
-          head_partial = !info_start(info);
-          const int g = info_hb(info) * W + w;
-          const T* qg = qbase + ((int64_t)info_row(info) * a.H_q + (int64_t)g * S) * D;
-          if constexpr (MF) {
-            mfma::begin_item<S>(ms, reinterpret_cast<const uint16_t*>(qg), lane);
-          } else {
-            const T* qp = qg + dl * Sh::VEC;
+          for (int j = 0; j < S; ++j) {
+            st.q[j] = *reinterpret_cast<const u32x4*>(qp + j * D);
+            st.m[j] = kMInit;
+            st.l[j] = 0.0f;
 #pragma unroll
-            for (int j = 0; j < S; ++j) {
-              st.q[j] = *reinterpret_cast<const u32x4*>(qp + j * D);
-              st.m[j] = kMInit;
-              st.l[j] = 0.0f;
-#pragma unroll
-              for (int e = 0; e < Sh::VEC; ++e) st.o[j][e] = 0.0f;
-            }
+            for (int e = 0; e < Sh::VEC; ++e) st.o[j][e] = 0.0f;
           }
         }
       }
-      issue(kr[(u + NBUF - 1) % NBUF], vr[(u + NBUF - 1) % NBUF], k + NBUF - 1);
-      if (pending) {  // wave-uniform
-        pending = false;
-        __builtin_amdgcn_s_waitcnt(kWaitRing);  // everything but the tile just issued
-        arrive(pend_x0, pend_x1, pend_row, pend_g);
-      }
-      if (k < n_units) {
+    }
+    return info;
+  };
+  // End of unit k (k < n_units): an item that ends here is finished in place
+  // when it lies wholly in the range; a part cut by the range stores its
+  // record and counts its arrival (at the next unit, or now at the range's
+  // last unit).
+  auto end_unit = [&](int k, int info) {
+    const bool tail_partial = k == n_units - 1 && !info_end(info);
+    if (info_end(info) || k == n_units - 1) {
+      const int r = info_row(info);
+      const int g = info_hb(info) * W + w;
+      T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)r * a.H_q + (int64_t)g * S) * D;
+      if (!head_partial && !tail_partial) {  // the whole item in this range
         if constexpr (MF)
-          mfma::fold<S>(ms, kr[u], vr[u], s_kv[w], lane, info_valid(info), a.scale_log2);
+          mfma::finish<S, T>(ms, lane, outp);
         else
-          fold_tile<T, D, S>(st, kr[u], vr[u], row, info_valid(info), a.scale_log2);
-        const bool tail_partial = k == n_units - 1 && !info_end(info);
-        if (info_end(info) || k == n_units - 1) {
-          const int r = info_row(info);
-          const int g = info_hb(info) * W + w;
-          T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)r * a.H_q + (int64_t)g * S) * D;
-          if (!head_partial && !tail_partial) {  // the whole item in this range
-            if constexpr (MF)
-              mfma::finish<S, T>(ms, lane, outp);
-            else
-              finish_rows<T, D, S>(st, row, dl, outp);
-          } else {  // (workgroup-uniform)
-            const int64_t slot = ((int64_t)bid * 2 + (head_partial ? 0 : 1)) * W + w;
-            if constexpr (MF)
-              mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
-            else
-              partial_rows<T, D, S>(st, row, dl, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
-            // the item's first and last units, and the ranges holding them
-            const int rr = info_row_seq(s_cum, R, a.nb, u0 + k);
-            const int np = s_cum[rr + 1] - s_cum[rr];
-            const int64_t e_first = (int64_t)a.nb * s_cum[rr] + (int64_t)info_hb(info) * np;
-            pend_x0 = range_of(e_first, U, G);
-            pend_x1 = range_of(e_first + np - 1, U, G);
-            pend_row = r;
-            pend_g = g;
-            if (k + 1 < n_units) {
-              pending = true;  // counted at the next unit
-            } else {
-              __builtin_amdgcn_s_waitcnt(0);  // the record stores have completed
-              arrive(pend_x0, pend_x1, pend_row, pend_g);
-            }
-          }
+          finish_rows<T, D, S>(st, row, dl, outp);
+      } else {  // (workgroup-uniform)
+        const int64_t slot = ((int64_t)bid * 2 + (head_partial ? 0 : 1)) * W + w;
+        if constexpr (MF)
+          mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
+        else
+          partial_rows<T, D, S>(st, row, dl, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
+        // the item's first and last units, and the ranges holding them
+        const int rr = info_row_seq(s_cum, R, a.nb, u0 + k);
+        const int np = s_cum[rr + 1] - s_cum[rr];
+        const int64_t e_first = (int64_t)a.nb * s_cum[rr] + (int64_t)info_hb(info) * np;
+        pend_x0 = range_of(e_first, U, G);
+        pend_x1 = range_of(e_first + np - 1, U, G);
+        pend_row = r;
+        pend_g = g;
+        if (k + 1 < n_units) {
+          pending = true;  // counted at the next unit
+        } else {
+          __builtin_amdgcn_s_waitcnt(0);  // the record stores have completed
+          arrive(pend_x0, pend_x1, pend_row, pend_g);
+        }
+      }
+    }
+  };
+  // (wait: the s_waitcnt encoding that leaves only the loads just issued
+  // outstanding, as a std::integral_constant)
+  auto arrive_pending = [&](auto wait) {
+    if (pending) {  // wave-uniform
+      pending = false;
+      __builtin_amdgcn_s_waitcnt(decltype(wait)::value);
+      arrive(pend_x0, pend_x1, pend_row, pend_g);
+    }
+  };
+
+  if constexpr (MF && kStreamSplitKV) {
+    // Matrix-core fold: a unit's K and V loads go out half a unit apart.  The
+    // K loads of unit k + 1 (after the queries of the item it starts, if it
+    // starts one) follow unit k's QK half, and its V loads follow unit k's PV
+    // half, before the unit's end (an output, or a record and maybe a merge);
+    // each is waited for about a unit after it was issued, so about one K and
+    // one V tile (8 KiB) are in flight per wave instead of two whole tiles,
+    // and one register set of each suffices.  These loads are issued as
+    // inline assembly, which the compiler's wait counting does not see (its
+    // own counting, across the merge paths, waited for every load at each
+    // unit), and are waited for explicitly: when unit k + 1's QK half starts,
+    // its V loads (NI instructions) went out after its K loads and queries,
+    // and when unit k's PV half starts, unit k + 1's K loads went out after
+    // unit k's V loads, so vmcnt(NI) suffices at both points whatever else
+    // (records, merges, outputs) went out in between.
+    static_assert(Sh::NI < 16, "vmcnt range");
+    const int n_q = lane & 15, g_q = lane >> 4;
+    auto load_queries = [&](int info) {
+      const int g = info_hb(info) * W + w;
+      const T* qg = qbase + ((int64_t)info_row(info) * a.H_q + (int64_t)g * S) * D;
+      // lane (n, G): row n of the group (zeros past the S rows), dims
+      // 32 s + 8 G .. +8 of Q^T operand s
+      asm_issue<mfma::kD / 32, 64>(scalar_rsrc(qg, S * D * 2), (n_q * D + g_q * 8) * 2, ms.qt);
+    };
+    auto tile_k = [&](int k, u32x4 (&x)[Sh::NI]) {
+      int64_t off;
+      int valid;
+      unit_tile(k, off, valid, true);
+      asm_issue<Sh::NI>(scalar_rsrc(kp + off, valid * D * (int)sizeof(T)), lane_off, x);
+    };
+    auto tile_v = [&](int k, u32x4 (&x)[Sh::NI]) {
+      int64_t off;
+      int valid;
+      unit_tile(k, off, valid, false);
+      asm_issue<Sh::NI>(scalar_rsrc(vp + off, valid * D * (int)sizeof(T)), lane_off, x);
+    };
+    u32x4 kc[Sh::NI], vc[Sh::NI];
+    load_queries(__builtin_amdgcn_readfirstlane(s_info[0]));
+    tile_k(0, kc);
+    tile_v(0, vc);
+    for (int k = 0; k < n_units; ++k) {
+      __syncthreads();  // lockstep, as in begin_unit
+      const int info = __builtin_amdgcn_readfirstlane(s_info[k]);
+      if (info_start(info) || k == 0) {
+        head_partial = !info_start(info);
+        mfma::reset<S>(ms);
+      }
+      vm_wait<Sh::NI>(kc);  // K of unit k and the queries (issued before it)
+      vm_wait<Sh::NI>(ms.qt);
+      mfma::s16x4_t phi, plo;
+      mfma::fold_qk<S>(ms, kc, s_kv[w], lane, info_valid(info), a.scale_log2, phi, plo);
+      if (k + 1 < n_units) {  // the queries are free once the QK half is done
+        const int next = __builtin_amdgcn_readfirstlane(s_info[k + 1]);
+        if (info_start(next)) load_queries(next);
+      }
+      tile_k(k + 1, kc);
+      arrive_pending(std::integral_constant<int, (Sh::NI & 15) | (7 << 4) | (15 << 8)>{});
+      vm_wait<Sh::NI>(vc);  // V of unit k
+      mfma::fold_pv<S>(ms, vc, s_kv[w], lane, phi, plo);
+      tile_v(k + 1, vc);
+      end_unit(k, info);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the last (null) tiles' loads
+  } else {
+    // A ring of NBUF register tiles: the tile of unit k + NBUF - 1 is issued
+    // at the start of unit k.
+    constexpr int kRingLoads = 2 * Sh::NI;  // load instructions of one issue()
+    constexpr int kWaitRing = (kRingLoads & 15) | (7 << 4) | (15 << 8) | ((kRingLoads >> 4) << 14);
+    static_assert(kRingLoads < 64, "vmcnt range");
+    u32x4 kr[NBUF][Sh::NI], vr[NBUF][Sh::NI];
+#pragma unroll
+    for (int u = 0; u + 1 < NBUF; ++u) issue(kr[u], vr[u], u);
+    for (int base = 0; base < n_units; base += NBUF) {
+#pragma unroll
+      for (int u = 0; u < NBUF; ++u) {
+        const int k = base + u;
+        const int info = begin_unit(k);
+        issue(kr[(u + NBUF - 1) % NBUF], vr[(u + NBUF - 1) % NBUF], k + NBUF - 1);
+        arrive_pending(std::integral_constant<int, kWaitRing>{});
+        if (k < n_units) {
+          if constexpr (MF)
+            mfma::fold<S>(ms, kr[u], vr[u], s_kv[w], lane, info_valid(info), a.scale_log2);
+          else
+            fold_tile<T, D, S>(st, kr[u], vr[u], row, info_valid(info), a.scale_log2);
+          end_unit(k, info);
         }
       }
     }

@@ -81,6 +81,43 @@ __device__ __forceinline__ void issue_tile(__amdgpu_buffer_rsrc_t rk, __amdgpu_b
   for (int i = 0; i < NI; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, lane_off, i * 1024, kKvLoadPolicy);
 }
 
+// The NI 16-byte-per-lane loads of one half (K or V) of a tile.
+template <int NI>
+__device__ __forceinline__ void issue_half(__amdgpu_buffer_rsrc_t r, int lane_off, u32x4 (&x)[NI]) {
+#pragma unroll
+  for (int i = 0; i < NI; ++i) x[i] = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, i * 1024, kKvLoadPolicy);
+}
+
+// Loads issued as inline assembly, for the stream kernel's split-KV loop:
+// the compiler's wait-count insertion does not see them, so its own waits
+// never drain them, and the caller waits for them with vm_wait.  rs is a
+// buffer descriptor in scalar registers (loads past num_records return
+// zeros); lane_off the lane's byte offset; load i reads STRIDE bytes
+// further on (a 1 KiB slice of a tile, or the next 32 dims of a query row).
+__device__ __forceinline__ u32x4 scalar_rsrc(const void* base, int num_bytes) {
+  const uint64_t p = (uint64_t)base;
+  return u32x4{(uint32_t)p, (uint32_t)(p >> 32) & 0xffffu, (uint32_t)num_bytes, 0x00020000u};
+}
+template <int NI, int STRIDE = 1024>
+__device__ __forceinline__ void asm_issue(const u32x4& rs, int lane_off, u32x4 (&x)[NI]) {
+  static_assert((NI - 1) * STRIDE < 4096, "immediate offset range");
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+    asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen offset:%3 nt"
+                 : "=v"(x[i])
+                 : "v"(lane_off), "s"(rs), "i"(i * STRIDE)
+                 : "memory");
+}
+// Wait until at most N vector-memory operations are outstanding, then hand
+// x to the code after the wait (the empty statements keep every use of x
+// below it).
+template <int N, int NI>
+__device__ __forceinline__ void vm_wait(u32x4 (&x)[NI]) {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
+#pragma unroll
+  for (int i = 0; i < NI; ++i) asm volatile("" : "+v"(x[i]));
+}
+
 // Fold one tile into the running state.  `valid` (wave-uniform) is the number
 // of live tokens in the tile; tokens at or past it get logit -inf (their V
 // was already read as 0 by the buffer range check), so whatever bytes the
@@ -294,16 +331,25 @@ struct State {
   float m, l;          // softmax base (log2 units, shared by the 4 lanes of a head) and partial sum
 };
 
+// An item's queries (the Q^T operand), and its fresh softmax state.
 template <int S>
-__device__ __forceinline__ void begin_item(State<S>& st, const uint16_t* q_group, int lane) {
+__device__ __forceinline__ void load_q(State<S>& st, const uint16_t* q_group, int lane) {
   const int n = lane & 15, G = lane >> 4;
 #pragma unroll
   for (int s = 0; s < kD / 32; ++s)
     st.qt[s] = n < S ? *reinterpret_cast<const u32x4*>(q_group + n * kD + s * 32 + G * 8) : u32x4{0, 0, 0, 0};
+}
+template <int S>
+__device__ __forceinline__ void reset(State<S>& st) {
 #pragma unroll
   for (int mb = 0; mb < kD / 16; ++mb) st.acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   st.m = kMInit;
   st.l = 0.0f;
+}
+template <int S>
+__device__ __forceinline__ void begin_item(State<S>& st, const uint16_t* q_group, int lane) {
+  load_q<S>(st, q_group, lane);
+  reset<S>(st);
 }
 
 // Split four fp32 softmax weights into bf16 high parts (round to nearest
@@ -335,18 +381,19 @@ __device__ __forceinline__ f32x4_t pv_mfma(const s16x4_t& va, const s16x4_t& phi
                                                  0, 0, 0);
 }
 
-// k / v: the tile as loaded (lane l: token l/16 + 4 i, 16-byte chunk l%16);
-// lds: this wave's 8 KiB (K then V); valid: live tokens of the tile.
+// The fold of one tile in two halves, so that a tile's V loads can be waited
+// for after its K half is done.  k / v: the tile as loaded (lane l: token
+// l/16 + 4 i, 16-byte chunk l%16); lds: this wave's 8 KiB (K then V); valid:
+// live tokens of the tile.
+//
+// fold_qk: K to LDS, S^T = K . Q^T, online softmax; the P^T operands (bf16
+// high and low parts of the lane's 4 weights) come back in phi / plo.
 template <int S>
-__device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u32x4 (&v)[4], uint8_t* lds, int lane,
-                                     int valid, float scale_log2) {
+__device__ __forceinline__ void fold_qk(State<S>& st, const u32x4 (&k)[4], uint8_t* lds, int lane, int valid,
+                                        float scale_log2, s16x4_t& phi, s16x4_t& plo) {
   const int G = lane >> 4, p = lane & 15;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int tok = G + 4 * i;
-    *reinterpret_cast<u32x4*>(lds + swz(tok, p)) = k[i];
-    *reinterpret_cast<u32x4*>(lds + kTile + swz_v(tok, p)) = v[i];
-  }
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(lds + swz(G + 4 * i, p)) = k[i];
   // S^T = K . Q^T
   f32x4_t s = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -377,9 +424,17 @@ __device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u3
 #pragma unroll
   for (int i = 0; i < 4; ++i) pw[i] = fast_exp2(fmaf(x[i], scale_log2, -st.m));
   st.l += (pw[0] + pw[1]) + (pw[2] + pw[3]);
-  s16x4_t phi, plo;
   split_hi_lo(pw, phi, plo);
-  // O^T += V^T . P^T; lane p of group G addresses token 4 G + p / 4, dims 16 mb + 4 (p % 4)
+}
+
+// fold_pv: V to LDS, O^T += V^T . P^T; lane p of group G addresses token
+// 4 G + p / 4, dims 16 mb + 4 (p % 4).
+template <int S>
+__device__ __forceinline__ void fold_pv(State<S>& st, const u32x4 (&v)[4], uint8_t* lds, int lane,
+                                        const s16x4_t& phi, const s16x4_t& plo) {
+  const int G = lane >> 4, p = lane & 15;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(lds + kTile + swz_v(G + 4 * i, p)) = v[i];
   const int vtok = 4 * G + (p >> 2);
 #pragma unroll
   for (int mb = 0; mb < kD / 16; ++mb) {
@@ -388,6 +443,15 @@ __device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u3
     const s16x4_t va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_s16x4_t*>(src));
     st.acc[mb] = pv_mfma(va, phi, plo, st.acc[mb]);
   }
+}
+
+// Both halves of one tile.
+template <int S>
+__device__ __forceinline__ void fold(State<S>& st, const u32x4 (&k)[4], const u32x4 (&v)[4], uint8_t* lds, int lane,
+                                     int valid, float scale_log2) {
+  s16x4_t phi, plo;
+  fold_qk<S>(st, k, lds, lane, valid, scale_log2, phi, plo);
+  fold_pv<S>(st, v, lds, lane, phi, plo);
 }
 
 // Totals of the head column of this lane: L summed over the 4 lane groups.
