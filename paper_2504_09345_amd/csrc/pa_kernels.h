@@ -83,8 +83,9 @@ constexpr int kStreamRing = PA_STREAM_RING;
 #ifndef PA_STREAM_SPLIT_KV
 #define PA_STREAM_SPLIT_KV 1
 #endif
-// Matrix-core fold: load a unit's K and V tiles half a unit apart (one tile
-// of each in flight per wave) rather than through the NBUF ring.
+// Stream-K kernel with the matrix-core fold: load a unit's K and V tiles
+// half a unit apart (about one tile of each in flight per wave) rather than
+// through the NBUF ring.  The mixed kernel keeps the ring.
 constexpr bool kStreamSplitKV = PA_STREAM_SPLIT_KV != 0;
 #ifndef PA_STREAM_MAX_WAVES
 #define PA_STREAM_MAX_WAVES 8

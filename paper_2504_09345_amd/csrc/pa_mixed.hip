@@ -34,7 +34,7 @@ template <int S, bool TR>
 __global__ __launch_bounds__(64 * kMixedW) void mixed_kernel(StreamArgs sa, PrefillArgs pa_, int G_dec) {
   __shared__ MixedSmem sm;
   if ((int)blockIdx.x < G_dec)
-    stream_body<uint16_t, mfma::kD, S, kMixedW, kStreamRing, true, TR>(sa, sm.dec, blockIdx.x, G_dec);
+    stream_body<uint16_t, mfma::kD, S, kMixedW, kStreamRing, true, TR, false>(sa, sm.dec, blockIdx.x, G_dec);
   else
     prefill_body<mfma::kD, S, TR>(pa_, sm.pf.smem, sm.pf.cum, blockIdx.x - G_dec, gridDim.x - G_dec);
 }

@@ -128,8 +128,11 @@ constexpr uint8_t kRowZeros = 0x20, kRowNaN = 0x40;
 
 // The stream-K decode workgroup `bid` of a grid of G (see pa_stream.hip).
 // TR: gather-trace instantiation (records every loaded token's pool row in
-// a.trace besides computing the attention).
-template <typename T, int D, int S, int W, int NBUF, bool MF, bool TR = false>
+// a.trace besides computing the attention).  SPLIT: with the matrix-core
+// fold, load K and V half a unit apart (the decode-only kernel); without it,
+// through the ring of NBUF whole tiles (the mixed kernel, whose decode
+// workgroups share HBM with prefill workgroups and need the longer lead).
+template <typename T, int D, int S, int W, int NBUF, bool MF, bool TR = false, bool SPLIT = kStreamSplitKV>
 __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, MF>& sm, int bid, int G_) {
   using Sh = DecodeShape<T, D, S>;
   constexpr int NT = 64 * W;
@@ -362,7 +365,7 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
     }
   };
 
-  if constexpr (MF && kStreamSplitKV) {
+  if constexpr (MF && SPLIT) {
     // Matrix-core fold: a unit's K and V loads go out half a unit apart.  The
     // K loads of unit k + 1 (after the queries of the item it starts, if it
     // starts one) follow unit k's QK half, and its V loads follow unit k's PV
