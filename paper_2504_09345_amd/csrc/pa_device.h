@@ -16,6 +16,7 @@ constexpr float kMInit = -1.0e30f;
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte lane load
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // Reinterpret one packed pair.  Takes the word by value: bit-casting an
 // ext-vector element lvalue directly (v.y) has been seen to read element 0.

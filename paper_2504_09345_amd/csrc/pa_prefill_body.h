@@ -13,7 +13,6 @@ using mfma::bf16x8_t;
 using mfma::f32x4_t;
 using mfma::lds_s16x4_t;
 using mfma::s16x4_t;
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));

@@ -76,6 +76,49 @@ __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64
   }
 }
 
+// The record of an item's other part, loaded ahead of merge_held: (M, L) and
+// the unnormalised O of this lane's head column in the matrix-core layout
+// (lanes of heads >= S load nothing).
+template <int S>
+struct HeldRecord {
+  float m = 0.0f, l = 0.0f;
+  float o[mfma::kD / 16][4] = {};
+};
+template <int S>
+__device__ __forceinline__ void load_held(HeldRecord<S>& r, const float* o, const float* ml, int lane) {
+  const int n = lane & 15, G = lane >> 4;
+  if (n < S) {
+    load_dev2(ml + n * 2, r.m, r.l);
+#pragma unroll
+    for (int mb = 0; mb < mfma::kD / 16; ++mb) {
+      load_dev2(o + n * mfma::kD + mb * 16 + 4 * G, r.o[mb][0], r.o[mb][1]);
+      load_dev2(o + n * mfma::kD + mb * 16 + 4 * G + 2, r.o[mb][2], r.o[mb][3]);
+    }
+  }
+}
+
+// merge_item for an item of two parts whose first part is this wave's
+// matrix-core state (its record never stored) and whose second part is the
+// record r: the same operations in the same order as merge_item over the two
+// records, so the output bits do not depend on which of the two parts merged.
+template <typename T, int S>
+__device__ __forceinline__ void merge_held(const mfma::State<S>& st, const HeldRecord<S>& r, int lane, T* out) {
+  const float l0 = mfma::total_l(st);  // (every lane: a cross-lane sum)
+  const int n = lane & 15, G = lane >> 4;
+  if (n < S) {
+    const float M = fmaxf(fmaxf(kMInit, st.m), r.m);
+    const float c0 = fast_exp2(st.m - M), c1 = fast_exp2(r.m - M);
+    const float L = fmaf(r.l, c1, fmaf(l0, c0, 0.0f));
+#pragma unroll
+    for (int mb = 0; mb < mfma::kD / 16; ++mb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        store_out<T>(out + n * mfma::kD + mb * 16 + 4 * G + i,
+                     fmaf(r.o[mb][i], c1, fmaf(st.acc[mb][i], c0, 0.0f)) / L);
+    }
+  }
+}
+
 // Count one part's arrival at an item's counter and return the parts counted
 // so far, this one included.  The counter's upper 48 bits carry the call's
 // token and its lower 16 bits the count: a counter left by an earlier call
@@ -286,6 +329,12 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
   int64_t pend_x0 = 0, pend_x1 = 0;
   int pend_row = 0, pend_g = 0;
 
+  // Range-end merge from registers (the matrix-core split loop sets these):
+  // the item ending the range has one other part, which has counted, and
+  // its record is in held_rec.
+  bool held_now = false;
+  HeldRecord<S> held_rec;
+
   // Start of unit k, every wave in step (without the barrier the older wave
   // of each SIMD runs ahead, waves 0..3 finish ~30% before waves 4..7, and
   // those then stream the rest alone with half the loads in flight; in step,
@@ -332,7 +381,13 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
           mfma::finish<S, T>(ms, lane, outp);
         else
           finish_rows<T, D, S>(st, row, dl, outp);
-      } else {  // (workgroup-uniform)
+      } else {  // (workgroup-uniform, but for merge_held)
+        if constexpr (MF) {
+          if (held_now && k == n_units - 1) {  // (wave-uniform)
+            merge_held<T, S>(ms, held_rec, lane, outp);
+            return;
+          }
+        }
         const int64_t slot = ((int64_t)bid * 2 + (head_partial ? 0 : 1)) * W + w;
         if constexpr (MF)
           mfma::partial<S>(ms, lane, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2);
@@ -401,9 +456,37 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
       unit_tile(k, off, valid, false);
       asm_issue<Sh::NI>(scalar_rsrc(vp + off, valid * D * (int)sizeof(T)), lane_off, x);
     };
+    //
+    // The range's last item, when cut by the range's end, usually finishes
+    // last: its other part started the next range and counted long before.
+    // If that item has two parts (it ends in the next range), its counter is
+    // loaded (inline assembly too) when the next-to-last unit's QK half
+    // starts, older than the K loads of the last unit, so the waits above
+    // cover it unchanged; it is looked at when the last unit starts; if the
+    // other part has counted, its record is loaded then, and the last unit
+    // ends by merging from registers (merge_held): no record stored, no
+    // arrival counted (every other part has counted, so no part reads the
+    // counter again in this call), the record's latency hidden behind the
+    // unit's fold.  With a single unit the counter load goes out between
+    // its K and V loads.
+    bool held = false;  // (wave-uniform) the range's last item qualifies
+    {
+      const int info_l = __builtin_amdgcn_readfirstlane(s_info[n_units - 1]);
+      if (!info_end(info_l)) {
+        const int rr = info_row_seq(s_cum, R, a.nb, u1 - 1);
+        const int np = s_cum[rr + 1] - s_cum[rr];
+        const int64_t e_first = (int64_t)a.nb * s_cum[rr] + (int64_t)info_hb(info_l) * np;
+        held = e_first >= u0 && range_of(e_first + np - 1, U, G) == bid + 1;
+      }
+    }
+    const unsigned long long* ctr_p = a.ws_flag + (int64_t)bid * W + w;
+    const unsigned long long counted = ((a.token & 0xffffffffffffull) << 16) | 1ull;  // one part counted
+    u32x2_t ctr = u32x2_t{0u, 0u};
+
     u32x4 kc[Sh::NI], vc[Sh::NI];
     load_queries(__builtin_amdgcn_readfirstlane(s_info[0]));
     tile_k(0, kc);
+    if (held && n_units == 1) asm_load_dev(ctr_p, ctr);
     tile_v(0, vc);
     for (int k = 0; k < n_units; ++k) {
       __syncthreads();  // lockstep, as in begin_unit
@@ -414,6 +497,16 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
       }
       vm_wait<Sh::NI>(kc);  // K of unit k and the queries (issued before it)
       vm_wait<Sh::NI>(ms.qt);
+      if (held && k + 2 == n_units) asm_load_dev(ctr_p, ctr);
+      if (held && k == n_units - 1) {
+        vm_wait<Sh::NI>(ctr);  // (issued before unit k's V loads)
+        held_now = __builtin_amdgcn_readfirstlane(ctr.x) == (uint32_t)counted &&
+                   __builtin_amdgcn_readfirstlane(ctr.y) == (uint32_t)(counted >> 32);
+        if (held_now) {
+          const int64_t slot = ((int64_t)(bid + 1) * 2 + 0) * W + w;
+          load_held<S>(held_rec, a.ws_o + slot * S * D, a.ws_ml + slot * S * 2, lane);
+        }
+      }
       mfma::s16x4_t phi, plo;
       mfma::fold_qk<S>(ms, kc, s_kv[w], lane, info_valid(info), a.scale_log2, phi, plo);
       if (k + 1 < n_units) {  // the queries are free once the QK half is done

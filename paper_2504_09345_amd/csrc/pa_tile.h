@@ -108,6 +108,12 @@ __device__ __forceinline__ void asm_issue(const u32x4& rs, int lane_off, u32x4 (
                  : "v"(lane_off), "s"(rs), "i"(i * STRIDE)
                  : "memory");
 }
+// One 8-byte load at p (the same address in every lane) with device scope,
+// as a relaxed device-scope atomic load is compiled, issued as inline
+// assembly like asm_issue's loads and waited for with vm_wait.
+__device__ __forceinline__ void asm_load_dev(const void* p, u32x2_t& x) {
+  asm volatile("global_load_dwordx2 %0, %1, off sc1" : "=v"(x) : "v"(p) : "memory");
+}
 // Wait until at most N vector-memory operations are outstanding, then hand
 // x to the code after the wait (the empty statements keep every use of x
 // below it).
@@ -116,6 +122,11 @@ __device__ __forceinline__ void vm_wait(u32x4 (&x)[NI]) {
   asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
 #pragma unroll
   for (int i = 0; i < NI; ++i) asm volatile("" : "+v"(x[i]));
+}
+template <int N>
+__device__ __forceinline__ void vm_wait(u32x2_t& x) {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "i"(N) : "memory");
+  asm volatile("" : "+v"(x));
 }
 
 // Fold one tile into the running state.  `valid` (wave-uniform) is the number
@@ -360,7 +371,6 @@ __device__ __forceinline__ void begin_item(State<S>& st, const uint16_t* q_group
 __device__ __forceinline__ void split_hi_lo(const float (&p)[4], s16x4_t& hi, s16x4_t& lo) {
   typedef float f32x2_t __attribute__((ext_vector_type(2)));
   typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
-  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
   const f32x2_t p01 = f32x2_t{p[0], p[1]}, p23 = f32x2_t{p[2], p[3]};
   const bf16x2v_t h01 = __builtin_convertvector(p01, bf16x2v_t);
   const bf16x2v_t h23 = __builtin_convertvector(p23, bf16x2v_t);

@@ -1,6 +1,7 @@
 """The decode kernel's split K/V loads are issued as inline assembly, which the
-compiler's wait counting does not see: the kernel must not read or write a
-load's destination registers before its own explicit wait.  This compiles
+compiler's wait counting does not see (the K/V tile, query and range-end
+counter loads): the kernel must not read or write a load's destination
+registers before its own explicit wait.  This compiles
 the stream-K kernels for gfx950 to assembly (no GPU needed) and checks, for
 every inline-assembly load of every matrix-core instantiation, that no
 instruction between the load and the next `s_waitcnt vmcnt` (in program text
@@ -30,16 +31,27 @@ def _regs(text):
 
 
 def _kernels(asm):
-    """(name, instruction lines) of each stream-K kernel with the matrix-core
-    fold (template argument MF = true: `...ELb1ELb0E...` or `...ELb1ELb1E...`)."""
+    """(name, instruction lines, indexes of the inline-assembly loads) of each
+    stream-K kernel with the matrix-core fold (template argument MF = true:
+    `...ELb1ELb0E...` or `...ELb1ELb1E...`).  Inline assembly sits between
+    `;;#ASMSTART` and `;;#ASMEND` in the compiler's output."""
     out = []
     for m in re.finditer(r"^(_ZN2pa13stream_kernel\w+):", asm, flags=re.M):
         name = m.group(1)
         if not re.search(r"Li2ELb1ELb[01]E", name):
             continue
         end = asm.index(".Lfunc_end", m.end())
-        body = [l.strip() for l in asm[m.end():end].splitlines()]
-        out.append((name, [l for l in body if l and not l.startswith(";")]))
+        lines, loads, in_asm = [], [], False
+        for l in (l.strip() for l in asm[m.end():end].splitlines()):
+            if l.startswith(";;#ASMSTART"):
+                in_asm = True
+            elif l.startswith(";;#ASMEND"):
+                in_asm = False
+            elif l and not l.startswith(";"):
+                if in_asm and re.match(r"(buffer|global)_load_", l):
+                    loads.append(len(lines))
+                lines.append(l)
+        out.append((name, lines, loads))
     return out
 
 
@@ -55,22 +67,66 @@ def stream_asm(tmp_path_factory):
     return open(out).read()
 
 
+_VM_OP = re.compile(r"(buffer|global|flat|scratch)_(load|store|atomic)")
+_BRANCH = re.compile(r"s_(c?branch)\w*\s+(\.LBB\w+)")
+
+
+def _untouched(lines, labels, loads, i, dst, counted=True):
+    """Follow every control-flow path from the load at line i until a wait
+    retires it and return the first line on the way that names a register of
+    dst, else None.  counted: a wait retires the load when it is `s_waitcnt
+    vmcnt(N)` with at least N vector-memory operations issued after the load
+    on that path (they retire in issue order); else any `s_waitcnt vmcnt`
+    ends the path."""
+    todo, seen = [(i + 1, 0)], set()
+    while todo:
+        j, younger = todo.pop()
+        while j < len(lines):
+            if (j, younger) in seen:
+                break
+            seen.add((j, younger))
+            t = lines[j]
+            m = re.match(r"s_waitcnt\b.*vmcnt\((\d+)\)", t)
+            if m and (younger >= int(m.group(1)) or not counted):
+                break  # retired on this path
+            if t.startswith("s_endpgm"):
+                break
+            if not t.startswith(".") and j not in loads and _regs(t) & dst:
+                return t
+            if _VM_OP.match(t):
+                younger = min(younger + 1, 64)
+            b = _BRANCH.match(t)
+            if b:
+                target = labels[b.group(2)]
+                if b.group(1) == "branch":
+                    j = target
+                    continue
+                todo.append((target, younger))
+            j += 1
+    return None
+
+
 def test_split_loads_are_untouched_until_their_wait(stream_asm):
     kernels = _kernels(stream_asm)
     assert kernels, "no matrix-core stream-K kernel in the assembly"
     checked = 0
-    for name, lines in kernels:
-        loads = [i for i, l in enumerate(lines) if l.startswith("buffer_load_dwordx4") and "offen offset:" in l]
+    counter_loads = 0
+    for name, lines, loads in kernels:
         assert loads, f"{name}: no inline-assembly loads (split K/V schedule not compiled in)"
-        for i in loads:
-            m = re.match(r"buffer_load_dwordx4 v\[(\d+):(\d+)\]", lines[i])
+        counter_loads += sum(lines[i].startswith("global_load_dwordx2") for i in loads)
+        labels = {m.group(1): j for j, l in enumerate(lines) if (m := re.match(r"(\.LBB\w+):", l))}
+        loads = set(loads)
+        for i in sorted(loads):
+            m = re.match(r"\w+ v\[(\d+):(\d+)\]", lines[i])
             dst = set(range(int(m.group(1)), int(m.group(2)) + 1))
-            for j in range(i + 1, len(lines)):
-                t = lines[j]
-                if t.startswith("s_waitcnt") and "vmcnt" in t:
-                    break
-                if t.startswith(".") or (t.startswith("buffer_load_dwordx4") and "offen offset:" in t):
-                    continue
-                assert not (_regs(t) & dst), f"{name}: `{t}` touches {lines[i]!r} before its wait"
+            # The range-end counter is loaded a unit before the unit that
+            # reads it; the static paths also run from its load straight into
+            # that read within one iteration (the unit index rules that out),
+            # so for it any wait ends a path; the tile and query loads are
+            # checked with the wait counts.
+            t = _untouched(lines, labels, loads, i, dst, counted=not lines[i].startswith("global_load"))
+            assert t is None, f"{name}: `{t}` touches {lines[i]!r} before its wait"
             checked += 1
     assert checked >= 20
+    # the range-end counter load of every instantiation (before the loop and in it)
+    assert counter_loads >= 2 * len(kernels)
