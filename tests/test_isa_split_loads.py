@@ -130,3 +130,59 @@ def test_split_loads_are_untouched_until_their_wait(stream_asm):
     assert checked >= 20
     # the range-end counter load of every instantiation (before the loop and in it)
     assert counter_loads >= 2 * len(kernels)
+
+
+def _check(text):
+    """_untouched over a hand-written instruction list: the first offending
+    line for each inline-assembly load (lines marked with a leading '*')."""
+    lines, loads = [], set()
+    for l in text.strip().splitlines():
+        l = l.strip()
+        if l.startswith("*"):
+            loads.add(len(lines))
+            l = l[1:].strip()
+        lines.append(l)
+    labels = {m.group(1): j for j, l in enumerate(lines) if (m := re.match(r"(\.LBB\w+):", l))}
+    out = []
+    for i in sorted(loads):
+        m = re.match(r"\w+ v\[(\d+):(\d+)\]", lines[i])
+        out.append(_untouched(lines, labels, loads, i, set(range(int(m.group(1)), int(m.group(2)) + 1))))
+    return out
+
+
+def test_checker_on_hand_written_paths():
+    # a use after a wait that retires the load passes; one before it fails
+    assert _check("""
+        *buffer_load_dwordx4 v[4:7], v1, s[0:3], 0 offen offset:0 nt
+        s_waitcnt vmcnt(0)
+        v_add_f32_e32 v8, v4, v5
+        s_endpgm""") == [None]
+    assert _check("""
+        *buffer_load_dwordx4 v[4:7], v1, s[0:3], 0 offen offset:0 nt
+        v_mov_b32_e32 v6, 0
+        s_waitcnt vmcnt(0)
+        s_endpgm""") == ["v_mov_b32_e32 v6, 0"]
+    # vmcnt(1) retires the older of two loads only
+    assert _check("""
+        *buffer_load_dwordx4 v[4:7], v1, s[0:3], 0 offen offset:0 nt
+        *buffer_load_dwordx4 v[8:11], v1, s[0:3], 0 offen offset:64 nt
+        s_waitcnt vmcnt(1)
+        v_add_f32_e32 v12, v4, v8
+        s_endpgm""") == [None, "v_add_f32_e32 v12, v4, v8"]
+    # a branch around the wait reaches the use
+    assert _check("""
+        *buffer_load_dwordx4 v[4:7], v1, s[0:3], 0 offen offset:0 nt
+        s_cbranch_scc1 .LBB0_2
+        s_waitcnt vmcnt(0)
+        .LBB0_2:
+        v_add_f32_e32 v12, v4, v4
+        s_endpgm""") == ["v_add_f32_e32 v12, v4, v4"]
+    # an unconditional branch skips the lines after it
+    assert _check("""
+        *buffer_load_dwordx4 v[4:7], v1, s[0:3], 0 offen offset:0 nt
+        s_branch .LBB0_3
+        v_mov_b32_e32 v4, 0
+        .LBB0_3:
+        s_waitcnt vmcnt(0)
+        v_mov_b32_e32 v4, 0
+        s_endpgm""") == [None]
