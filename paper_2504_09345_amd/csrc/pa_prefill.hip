@@ -21,10 +21,12 @@
 // 2^-11 relative (bf16 P alone missed the relative tolerance; fp16 P adds a
 // tenth of what the bf16 rounding of the output costs), and bf16 V converts
 // to fp16 exactly for magnitudes in [2^-17, 2^16).  An item whose V holds a
-// value of 2^16 or more (or inf / NaN), or whose output rows have an RMS
-// below 2^-14 (where fp16's subnormal V could matter), is computed again in
-// a bf16 pass: V as loaded, P as its bf16 high and low parts in two
-// v_mfma_f32_16x16x32_bf16 (fp32-level accuracy).
+// value of 2^16 or more (or inf / NaN; in fp16 each makes every row of the
+// item non-finite), or whose output rows have an RMS below 2^-14 (where
+// fp16's subnormal V could matter), is computed again in a bf16 pass: V as
+// loaded, P as its bf16 high and low parts in two v_mfma_f32_16x16x32_bf16
+// (fp32-level accuracy).  Both conditions are read off the first pass's
+// output rows.
 // Computing the transposed products keeps "lane l % 16 = query row" in every
 // accumulator, so the softmax statistics, the P operand and the O rescale all
 // stay in the lane that owns the row: no register transposes.

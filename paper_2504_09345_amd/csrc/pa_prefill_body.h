@@ -37,7 +37,7 @@ struct PrefillSmem {
   __attribute__((aligned(16))) uint8_t v[kPfLdsSteps][kPfStep * kPage * mfma::kD * 2];
   int32_t bt[kPfMaxPages];
   int32_t scan[kPfThreads];
-  int32_t vwide;  // the item needs the bf16 pass (V outside the fp16 range, or tiny output rows)
+  int32_t vwide;  // the item needs the bf16 pass (non-finite or tiny output rows after the fp16 pass)
 };
 
 // Prefill workgroup `bid` of a grid of G; s_cum holds B + 1 ints of LDS.
@@ -174,22 +174,22 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
     };
     // With F16, V is staged as fp16: bf16 magnitudes in [2^-17, 2^16) and
     // zeros convert exactly, smaller ones to fp16 subnormals (absolute error
-    // <= 2^-25); a chunk with a larger, infinite or NaN value marks the item,
-    // which is then run again in bf16.
+    // <= 2^-25), larger ones to infinity (the largest bf16 below 2^16, 65280,
+    // is an fp16 value).  A value that is not finite in fp16 makes every row
+    // of the item non-finite (a weight times infinity or NaN, and 0 times
+    // either is NaN), which the check after the pass catches; the item then
+    // runs again in bf16.
     auto stash = [&](auto f16, int t, const u32x4& kr, const u32x4& vr) {
       const int buf = t % kPfLdsSteps;
       *reinterpret_cast<u32x4*>(s_k[buf] + st_off) = kr;
       if constexpr (decltype(f16)::value) {
         u32x4 vh;
-        uint32_t mx = 0;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const f32x2_t f = f32x2_t{__uint_as_float(vr[i] << 16), __uint_as_float(vr[i] & 0xffff0000u)};
           vh[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2_t));
-          mx = max(mx, max(vr[i] & 0x7fffu, (vr[i] >> 16) & 0x7fffu));
         }
         *reinterpret_cast<u32x4*>(s_v[buf] + st_off_v) = vh;
-        if (mx >= 0x4780u) sm.vwide = 1;  // |v| >= 2^16, inf or NaN
       } else {
         *reinterpret_cast<u32x4*>(s_v[buf] + st_off_v) = vr;
       }
@@ -408,8 +408,11 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
       if constexpr (decltype(f16)::value) {
         // fp16 V is exact for bf16 magnitudes in [2^-17, 2^16); smaller ones
         // carry an absolute error <= 2^-25, which stays below a tenth of the
-        // relative tolerance only for rows whose output RMS is >= 2^-14
-        bool tiny = false;
+        // relative tolerance only for rows whose output RMS is >= 2^-14;
+        // larger ones (and infinities, NaNs) leave the rows non-finite.
+        // Either marks the item for the bf16 pass (so does a NaN or infinite
+        // K, whose rows are non-finite in both passes).
+        bool redo = false;
 #pragma unroll
         for (int rb = 0; rb < kPfBlocks; ++rb) {
           const float inv = 1.0f / acc_l[rb][0];
@@ -418,17 +421,17 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs& a, PrefillSmem& 
           for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) ss = fmaf(acc[rb][mb][i] * inv, acc[rb][mb][i] * inv, ss);
-          // ss of the row's D dims (a NaN row is left as it is)
+          // ss of the row's D dims
           const float row_ss = rows4_sum(ss);
-          tiny |= lim[rb] >= 0 && row_ss < (float)D * 0x1p-28f;
+          redo |= lim[rb] >= 0 && !(row_ss >= (float)D * 0x1p-28f && row_ss <= __FLT_MAX__);
         }
-        if (__builtin_amdgcn_ballot_w64(tiny) != 0 && lane == 0) sm.vwide = 1;
+        if (__builtin_amdgcn_ballot_w64(redo) != 0 && lane == 0) sm.vwide = 1;
       }
     };
     // fp16 pass; an item whose V does not fit fp16 (or whose output rows are
     // too small for fp16's subnormal V) is recomputed in bf16
     pipeline(PfBool<true>{});
-    __syncthreads();  // every stash of the pass has set or left the flag
+    __syncthreads();  // every wave's check of the pass has set or left the flag
     if (sm.vwide) {
       if (npg > kPfMaxPages) {  // the pass slid the block-table window: back to page 0
         for (int i = tid; i < kPfMaxPages; i += kPfThreads) s_bt[i] = bt.page(b, i);
