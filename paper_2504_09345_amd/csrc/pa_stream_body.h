@@ -287,18 +287,6 @@ __device__ __forceinline__ void stream_body(const StreamArgs& a, StreamSmem<W, M
     unit_tile(k, off, valid, true);
     issue_tile<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), tile_rsrc<T, D>(vp + off, valid), lane_off, kr, vr);
   };
-  auto issue_k = [&](u32x4 (&kr)[Sh::NI], int k) {
-    int64_t off;
-    int valid;
-    unit_tile(k, off, valid, true);
-    issue_half<Sh::NI>(tile_rsrc<T, D>(kp + off, valid), lane_off, kr);
-  };
-  auto issue_v = [&](u32x4 (&vr)[Sh::NI], int k) {
-    int64_t off;
-    int valid;
-    unit_tile(k, off, valid, false);
-    issue_half<Sh::NI>(tile_rsrc<T, D>(vp + off, valid), lane_off, vr);
-  };
 
   // Items cut by range boundaries.  Every part (the item's first part ends
   // its range; a later part starts one) stores its partial record, then

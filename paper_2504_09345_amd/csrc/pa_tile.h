@@ -81,13 +81,6 @@ __device__ __forceinline__ void issue_tile(__amdgpu_buffer_rsrc_t rk, __amdgpu_b
   for (int i = 0; i < NI; ++i) v[i] = __builtin_amdgcn_raw_buffer_load_b128(rv, lane_off, i * 1024, kKvLoadPolicy);
 }
 
-// The NI 16-byte-per-lane loads of one half (K or V) of a tile.
-template <int NI>
-__device__ __forceinline__ void issue_half(__amdgpu_buffer_rsrc_t r, int lane_off, u32x4 (&x)[NI]) {
-#pragma unroll
-  for (int i = 0; i < NI; ++i) x[i] = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off, i * 1024, kKvLoadPolicy);
-}
-
 // Loads issued as inline assembly, for the stream kernel's split-KV loop:
 // the compiler's wait-count insertion does not see them, so its own waits
 // never drain them, and the caller waits for them with vm_wait.  rs is a
@@ -485,37 +478,6 @@ __device__ __forceinline__ void finish(const State<S>& st, int lane, T* out) {
       *reinterpret_cast<uint2*>(out + n * kD + d) = make_uint2(lo, hi);
     }
   }
-}
-
-// Fold another range's partial record of the same item (unnormalised O
-// [s][D] and (M, L) per head, device-coherent loads) into the state: one
-// log-sum-exp merge step.  Afterwards the state's L is the item total so far.
-template <int S>
-__device__ __forceinline__ void merge_record(State<S>& st, const float* o, const float* ml, int lane) {
-  const int n = lane & 15, G = lane >> 4;
-  float L = total_l(st);
-  float mx = kMInit, lx = 0.0f;
-  f32x4_t ox[kD / 16];
-#pragma unroll
-  for (int mb = 0; mb < kD / 16; ++mb) ox[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  if (n < S) {
-    load_dev2(ml + n * 2, mx, lx);
-#pragma unroll
-    for (int mb = 0; mb < kD / 16; ++mb) {
-      const int d = mb * 16 + 4 * G;
-      float x0, x1, x2, x3;
-      load_dev2(o + n * kD + d, x0, x1);
-      load_dev2(o + n * kD + d + 2, x2, x3);
-      ox[mb] = f32x4_t{x0, x1, x2, x3};
-    }
-  }
-  const float M = fmaxf(st.m, mx);
-  const float c0 = fast_exp2(st.m - M), c1 = fast_exp2(mx - M);
-#pragma unroll
-  for (int mb = 0; mb < kD / 16; ++mb) st.acc[mb] = st.acc[mb] * c0 + ox[mb] * c1;
-  L = fmaf(L, c0, lx * c1);
-  st.m = M;
-  st.l = L * 0.25f;  // the 4 lanes of a head each hold a quarter (exact)
 }
 
 // Partial record: unnormalised O [s][D] and (M, L) per head (device-coherent
