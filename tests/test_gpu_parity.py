@@ -200,6 +200,24 @@ def test_full_size_prefill_alone():
     assert_parity(got, ref, strict=False, what="prefill-8x512")
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("name,seed", [("mixtral-256", 1), ("dbrx-512", 3)])
+def test_full_size_decode_repeats_bit_identically(name, seed):
+    """An item cut by a range boundary is merged by whichever of its parts
+    finishes last: the range's end part from its registers when the other
+    part has already counted, otherwise the last part to count, from the
+    stored records, with the same operations in the same order.  Which part
+    merges depends on timing, so repeated launches of the full batch must
+    give the same bits."""
+    announce(f"full {name} seed={seed}: repeated launches")
+    b = _full(name, seed)
+    dev = upload(b)
+    first = run_gpu(b, dev=dev)
+    for i in range(16):
+        again = run_gpu(b, dev=dev)
+        assert np.array_equal(first.view(np.uint32), again.view(np.uint32)), (name, i)
+
+
 # --- stream-K vs split-K ----------------------------------------------------
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
