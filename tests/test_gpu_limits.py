@@ -2,7 +2,8 @@
 choice (H_kv = 1, 2, 4, 8 and 16, i.e. W = 1, 2, 4, 8 and two head blocks),
 a batch whose per-workgroup ranges reach the LDS unit-table limit (the grid
 grows past three quarters of the CUs), and a batch one sequence past the
-stream tables (split-K path).  Sizes keep the oracle to sampled sequences."""
+stream tables (split-K path), and batches with ranges of one unit or none.
+Sizes keep the oracle to sampled sequences where they are large."""
 import numpy as np
 import pytest
 
@@ -64,3 +65,20 @@ def test_batch_past_the_stream_tables_takes_split_k():
     seqs = list(range(0, 8193, 431)) + [8192]
     sb, rows = sub_batch(b, seqs)
     assert_parity(got[rows], run_oracle(sb), what="B=8193")
+
+
+@pytest.mark.parametrize("B,lo,hi", [(104, 33, 48), (70, 17, 32), (150, 17, 48)])
+def test_ranges_of_one_unit_or_none(B, lo, hi):
+    """Batches with fewer units than twice the grid (Mixtral shape, two or
+    three pages per sequence): ranges of one unit, empty ranges, and items
+    of two or three units cut at every range boundary, so a range's only
+    unit can be the first part of a two-part item (its counter read before
+    the loop) and a cut item can skip an empty range.  Every row against the
+    oracle, and the same bits on a second launch."""
+    announce(f"one-unit ranges B={B} ctx {lo}..{hi}")
+    b = W.generate("mixtral-256", seed=B, overrides=dict(B=B, ctx=("uniform", lo, hi)))
+    units = int(((b.context_lens + 15) // 16).sum())
+    assert units < 2 * 208
+    got = run_gpu(b)
+    assert_parity(got, run_oracle(b), what=f"one-unit ranges B={B}")
+    assert np.array_equal(got.view(np.uint32), run_gpu(b).view(np.uint32))
