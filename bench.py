@@ -55,6 +55,7 @@ WORKLOAD_NAMES = {
     "dbrx-512": "dbrx-decode-b512-lognormal-ctx128-8192",
     "mixed": "mixtral-8x7b-mixed-8x512prefill-512decode",
     "prefill-8x512": "mixtral-8x7b-prefill-8x512",
+    "prefill-16x2048": "mixtral-8x7b-prefill-16x2048",
     "tiny": "tiny-decode-b4",
 }
 

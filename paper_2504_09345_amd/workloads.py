@@ -56,6 +56,10 @@ CONFIGS = {
     # the same 8 prefill chunks on their own (the chunked-prefill kernel alone)
     "prefill-8x512": dict(kind="varlen", H_q=32, H_kv=8, D=128, prefill=(8, 512, 0, 1536),
                           decode=(0, 256, 4096), pool=("factor", 1.25), std=0.5),
+    # a prefill-heavy step: 16 causal chunks of 2048 rows over 0..2048 cached
+    # tokens, the chunked-prefill kernel alone
+    "prefill-16x2048": dict(kind="varlen", H_q=32, H_kv=8, D=128, prefill=(16, 2048, 0, 2048),
+                            decode=(0, 256, 4096), pool=("factor", 1.25), std=0.5),
 }
 
 

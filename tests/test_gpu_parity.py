@@ -201,6 +201,23 @@ def test_full_size_prefill_alone():
 
 
 @pytest.mark.slow
+def test_full_size_prefill_heavy_sampled():
+    """16 chunks of 2,048 rows on 2,048-4,096 tokens, as the benchmark's
+    prefill-heavy workload times them (the chunked-prefill kernel alone, 16
+    items per workgroup): the shortest, the longest and two more
+    sequences, every row of each (8,192 rows), against the oracle."""
+    announce("full prefill-16x2048 seed=1: generate")
+    b = _full("prefill-16x2048", 1)
+    assert b.num_seqs == 16 and int(b.q_lens.min()) == 2048
+    announce(f"full prefill-16x2048: gpu run rows={b.num_q_rows}")
+    got = run_gpu(b)
+    lens = b.context_lens
+    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), 0, 9})
+    sb, rows = sub_batch(b, seqs)
+    assert_parity(got[rows], run_oracle(sb), strict=False, what="prefill-16x2048")
+
+
+@pytest.mark.slow
 @pytest.mark.parametrize("name,seed", [("mixtral-256", 1), ("dbrx-512", 3)])
 def test_full_size_decode_repeats_bit_identically(name, seed):
     """An item cut by a range boundary is merged by whichever of its parts

@@ -37,7 +37,8 @@ def test_tiny_matches_its_description():
     assert used.min() >= 0 and used.max() < 64
 
 
-@pytest.mark.parametrize("name", ["mixtral-256", "long-ctx-64", "dbrx-512", "mixed", "prefill-8x512"])
+@pytest.mark.parametrize("name", ["mixtral-256", "long-ctx-64", "dbrx-512", "mixed", "prefill-8x512",
+                                  "prefill-16x2048"])
 def test_length_mixes(name):
     # only the small draws: lengths and the page permutation (patch the bulk draw)
     orig = W._fill_normal
@@ -63,6 +64,9 @@ def test_length_mixes(name):
     if name == "prefill-8x512":
         assert (b.q_lens == 512).all() and len(ctx) == 8
         assert (ctx >= 512).all() and (ctx <= 2048).all()
+    if name == "prefill-16x2048":
+        assert (b.q_lens == 2048).all() and len(ctx) == 16
+        assert (ctx >= 2048).all() and (ctx <= 4096).all()
     need = int(((ctx + 15) // 16).sum())
     assert b.meta["pages_used"] == need
     # pool sized 1.25x the need, pages disjoint
