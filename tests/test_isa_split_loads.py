@@ -55,13 +55,15 @@ def _kernels(asm):
     return out
 
 
-@pytest.fixture(scope="module")
-def stream_asm(tmp_path_factory):
+@pytest.fixture(scope="module", params=["pa_stream.hip", "pa_trace.hip"])
+def stream_asm(request, tmp_path_factory):
+    """The production stream-K kernels and their gather-trace instantiations
+    (which the bit-exact gather test runs)."""
     if not os.path.exists(build.HIPCC):
         pytest.skip("hipcc not available")
-    out = tmp_path_factory.mktemp("isa") / "pa_stream.s"
+    out = tmp_path_factory.mktemp("isa") / (request.param + ".s")
     cmd = [build.HIPCC, *build.FLAGS, "--cuda-device-only", "-S",
-           os.path.join(build.CSRC, "pa_stream.hip"), "-o", str(out)]
+           os.path.join(build.CSRC, request.param), "-o", str(out)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     return open(out).read()
