@@ -25,14 +25,19 @@ __device__ __forceinline__ int info_row(int i) { return (int)((unsigned)i >> 13)
 // lane, records merged in range order.  Every part of the item stores its
 // record before it counts its arrival, and whichever part arrives last runs
 // this merge over all the records, so the result does not depend on which
-// range merges.
+// range merges.  When a lane's E elements lie in one head (D a multiple of
+// E), the lane keeps only that head's running (M, L); the arithmetic of each
+// element is the same either way.
 template <typename T, int D, int S, int W>
 __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64_t G, int64_t wg_first,
                                            int64_t wg_last, int w, int lane, T* out) {
   constexpr int E = S * D / 64;  // elements per lane
-  float M[S], L[S], acc[E];
+  constexpr bool kOneHead = D % E == 0;
+  constexpr int NH = kOneHead ? 1 : S;  // heads whose (M, L) the lane keeps
+  const int h0 = kOneHead ? lane * E / D : 0;
+  float M[NH], L[NH], acc[E];
 #pragma unroll
-  for (int j = 0; j < S; ++j) { M[j] = kMInit; L[j] = 0.0f; }
+  for (int j = 0; j < NH; ++j) { M[j] = kMInit; L[j] = 0.0f; }
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.0f;
   // pass 1: maxima
@@ -40,17 +45,17 @@ __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64
     if (U * x / G == U * (x + 1) / G) continue;  // empty range wrote nothing
     const int64_t slot = (x * 2 + (x == wg_first ? 1 : 0)) * W + w;
 #pragma unroll
-    for (int j = 0; j < S; ++j) M[j] = fmaxf(M[j], load_dev(a.ws_ml + slot * S * 2 + j * 2));
+    for (int j = 0; j < NH; ++j) M[j] = fmaxf(M[j], load_dev(a.ws_ml + slot * S * 2 + (h0 + j) * 2));
   }
   // pass 2: weighted sums
   for (int64_t x = wg_first; x <= wg_last; ++x) {
     if (U * x / G == U * (x + 1) / G) continue;
     const int64_t slot = (x * 2 + (x == wg_first ? 1 : 0)) * W + w;
-    float c[S];
+    float c[NH];
 #pragma unroll
-    for (int j = 0; j < S; ++j) {
+    for (int j = 0; j < NH; ++j) {
       float m, l;
-      load_dev2(a.ws_ml + slot * S * 2 + j * 2, m, l);
+      load_dev2(a.ws_ml + slot * S * 2 + (h0 + j) * 2, m, l);
       c[j] = fast_exp2(m - M[j]);
       L[j] = fmaf(l, c[j], L[j]);
     }
@@ -66,13 +71,13 @@ __device__ __forceinline__ void merge_item(const StreamArgs& a, int64_t U, int64
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int idx = lane * E + e;
-      acc[e] = fmaf(v[e], c[idx / D], acc[e]);
+      acc[e] = fmaf(v[e], c[idx / D - h0], acc[e]);
     }
   }
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int idx = lane * E + e;
-    store_out<T>(out + idx, acc[e] / L[idx / D]);
+    store_out<T>(out + idx, acc[e] / L[idx / D - h0]);
   }
 }
 
