@@ -19,13 +19,16 @@
 //    item continues past the range).  Each part counts its arrival at the
 //    item's counter once its record is stored; the last part to arrive merges
 //    every record in range order (deterministic, no float atomics, and no
-//    workgroup ever waits for another): one launch per call.
+//    workgroup ever waits for another): one launch per call.  A range whose
+//    last item has one other part that has already counted merges it from
+//    registers with that part's record, in the same order and arithmetic.
 //
 // Per workgroup: prefix sums of page counts over all rows (LDS), then a unit
-// table for its range (page id and flags per unit, LDS), then each wave runs
-// a ring of NBUF register tile buffers over the units, exactly as in the
-// split kernel's inner loop, with a workgroup barrier per unit to keep the
-// waves in step.
+// table for its range (page id and flags per unit, LDS), then the units in
+// order, with a workgroup barrier per unit to keep the waves in step.  With
+// the matrix-core fold (bf16, head dim 128) each wave loads a unit's K and V
+// tiles half a unit apart, one register set each; otherwise it runs a ring
+// of NBUF whole-tile register buffers, as the split kernel's inner loop does.
 #include "pa_stream_kernel.h"
 
 namespace pa {
