@@ -57,6 +57,25 @@ def test_append_varlen_bit_exact(dtype):
     assert np.array_equal(_host(dev["v"], dtype), ev)
 
 
+def test_append_varlen_many_sequences_bit_exact():
+    """16,400 sequences in a varlen call: past the 16,383 whose
+    query_start_loc the kernel stages in LDS, the rows find their sequence in
+    global memory instead (two chunks among single-row sequences)."""
+    announce("kv append varlen 16400 sequences")
+    b = W.generate("mixed", seed=13, overrides=dict(
+        prefill=(2, 40, 0, 60), decode=(16398, 1, 40), H_q=4, H_kv=1, D=64))
+    assert b.num_seqs == 16400
+    T = int(b.query_start_loc[-1])
+    kn = _new_rows(T, b.num_kv_heads, b.head_dim, "bf16", 3)
+    vn = _new_rows(T, b.num_kv_heads, b.head_dim, "bf16", 4)
+    ek, ev = oracle.kv_append(kn, vn, b.block_table, b.context_lens, b.k_pages, b.v_pages,
+                              query_start_loc=b.query_start_loc)
+    dev = upload(b)
+    _append_gpu(b, kn, vn, dev, varlen=True)
+    assert np.array_equal(_host(dev["k"], "bf16"), ek)
+    assert np.array_equal(_host(dev["v"], "bf16"), ev)
+
+
 @pytest.mark.parametrize("D", [64, 128])
 def test_append_decode_layout_bit_exact(D):
     announce(f"kv append decode D={D}")
